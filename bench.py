@@ -1,0 +1,459 @@
+#!/usr/bin/env python3
+"""Benchmark of the paged prefix-reuse attention hot path on one MI355X.
+
+One step = one downstream-operator pass over the Llama-3-8B-shaped prefix-reuse workload
+(256 tuples, 32 query / 8 kv heads, head_dim 128, cached prefix U[256,1024], new tokens
+U[64,256], 40k-block pool with random placement):
+    kv_append (the new tokens)  ->  prefill attention (new tokens over prefix + suffix)
+    kv_append (one decode token per tuple)  ->  decode attention (split-K + merge)
+Block tables come from the library's allocator (checked equal to the generator's placement)
+and are resident in HBM with every input before the timed region starts.
+
+Prints ONE JSON line: value = tuples per second per attention layer for the whole step, plus
+the per-kernel figures, the roofline of the dominant kernel (prefill: bf16 matrix cores),
+the CPU oracle timed on a bounded sample of the same workload, and secondary workloads
+(paged decode, the mixed 70B-shaped batch, long documents with a shared prompt).
+
+    python bench.py [--steps K] [--warmup W] [--no-secondary] [--no-cpu-baseline]
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 matrix-core peak (256 CU x 2.4 GHz x 4096)
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E peak
+METRIC = "prefill TFLOP/s (% MFMA peak) + decode HBM GB/s (% peak); tuples/s per layer"
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------------------------------
+# algorithmic work ("Measurement")
+# ---------------------------------------------------------------------------------------
+def prefill_flops(prefix, new, hq, d):
+    p = prefix.astype(np.float64)
+    n = new.astype(np.float64)
+    return float(4.0 * d * hq * np.sum(n * p + n * (n + 1) / 2.0))
+
+
+def prefill_bytes(prefix, new, hq, hkv, d):
+    keys = (prefix + new).astype(np.float64)
+    kv = np.sum(keys) * hkv * d * 2 * 2
+    qo = np.sum(new) * hq * d * 2 * 2
+    return float(kv + qo)
+
+
+def decode_bytes(seq_lens, hq, hkv, d):
+    kv = np.sum(seq_lens.astype(np.float64)) * hkv * d * 2 * 2
+    qo = len(seq_lens) * hq * d * 2 * 2
+    return float(kv + qo)
+
+
+def append_bytes(total_new, hkv, d):
+    return float(total_new * hkv * d * 2 * 2 * 2)  # K and V, read + write
+
+
+def source_hash(*names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2607_23815_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+KERNEL_SOURCES = {
+    "prefill": ("prefill.hip", "device_utils.h"),
+    "decode": ("decode.hip", "device_utils.h"),
+    "append": ("kv_copy.hip", "device_utils.h"),
+}
+
+
+def traffic_from_profiles(kernel):
+    """HBM bytes per launch from the committed counter summary, if it was taken on the
+    current kernel source; otherwise None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        data = json.load(f)
+    ent = data.get(kernel)
+    if not ent or ent.get("source_hash") != source_hash(*KERNEL_SOURCES[kernel]):
+        return None
+    return ent.get("hbm_bytes_per_launch")
+
+
+# ---------------------------------------------------------------------------------------
+# workload set-up
+# ---------------------------------------------------------------------------------------
+class Workload:
+    """A generated workload on the device, with tables from the library's allocator."""
+
+    def __init__(self, spec, lib, torch):
+        import workloads as W
+        from tests.gpu_util import i32
+        t0 = time.time()
+        case = W.plan_case(spec)
+        W.fill_device(case, "cuda")
+        self.spec, self.case = spec, case
+        self.hq, self.hkv, self.d = spec.num_q_heads, spec.num_kv_heads, spec.head_dim
+        self.scale = 1.0 / math.sqrt(self.d)
+        # allocator: same placement order; the upstream operator's prefix is committed, the
+        # downstream suffix reserved
+        t_alloc = time.perf_counter()
+        pool = lib.BlockPool(case.num_blocks, spec.block_size, free_order=case.free_order)
+        parent = None
+        if spec.shared_prompt_tokens:
+            parent = pool.create()
+            pool.reserve(parent, spec.shared_prompt_tokens)
+            pool.commit(parent, spec.shared_prompt_tokens)
+        self.batches = []
+        for b in case.batches:
+            sids = []
+            for k in range(b.n_seqs):
+                if parent is not None:
+                    s = pool.fork(parent, spec.shared_prompt_tokens)
+                    st = pool.reserve(s, int(b.prefix_lens[k]) - spec.shared_prompt_tokens)
+                else:
+                    s = pool.create()
+                    st = pool.reserve(s, int(b.prefix_lens[k]))
+                assert st == lib.PKV_OK
+                pool.commit(s, int(b.prefix_lens[k]) - (spec.shared_prompt_tokens
+                                                        if parent is not None else 0))
+                assert pool.reserve(s, int(b.new_lens[k])) == lib.PKV_OK
+                sids.append(s)
+            tables, lens = pool.block_tables(sids, b.max_blocks)
+            assert np.array_equal(tables, b.block_tables), "allocator != generator placement"
+            assert np.array_equal(lens, b.prefix_lens)
+            self.batches.append((b, sids))
+        self.alloc_s = time.perf_counter() - t_alloc
+        self.pool = pool
+        self.parent = parent
+        self.dev = []
+        for b, _ in self.batches:
+            self.dev.append(dict(tables=i32(b.block_tables), cached=i32(b.prefix_lens),
+                                 cu=i32(b.cu_new_lens),
+                                 max_new=int(b.new_lens.max()) if b.n_seqs else 0,
+                                 max_total=int((b.prefix_lens + b.new_lens).max())
+                                 if b.n_seqs else 0))
+        torch.cuda.synchronize()
+        self.setup_s = time.time() - t0
+
+    def decode_followup(self, bi, lib, torch):
+        """Tables etc. for one decode step after the prefill: commit the suffix, reserve one
+        token per tuple (the allocator adds a block where a tuple's length is a multiple of
+        16), and draw that token's q/k/v."""
+        from tests.gpu_util import i32
+        b, sids = self.batches[bi]
+        for k, s in enumerate(sids):
+            self.pool.commit(s, int(b.new_lens[k]))
+            assert self.pool.reserve(s, 1) == lib.PKV_OK
+        ctx = (b.prefix_lens + b.new_lens).astype(np.int32)
+        mb = int(-(-(ctx + 1).max() // 16))
+        tables, lens = self.pool.block_tables(sids, mb)
+        assert np.array_equal(lens, ctx)
+        g = torch.Generator(device="cuda")
+        g.manual_seed(self.case.seed + 7)
+        nseq = b.n_seqs
+
+        def rnd(*shape):
+            return torch.randn(*shape, generator=g, device="cuda").to(torch.bfloat16)
+
+        return dict(tables=i32(tables), ctx=i32(ctx), seq_lens=i32(ctx + 1),
+                    cu=i32(np.arange(nseq + 1)), max_len=int(ctx.max()) + 1,
+                    q=rnd(nseq, self.hq, self.d), k=rnd(nseq, self.hkv, self.d),
+                    v=rnd(nseq, self.hkv, self.d), host_tables=tables, host_ctx=ctx)
+
+
+def time_events(torch, stream, fns, steps, warmup):
+    """Run the list of callables `steps` times after `warmup`, with an event before and
+    after each; returns (total seconds, per-callable mean seconds)."""
+    for _ in range(warmup):
+        for f in fns:
+            f()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)]
+          for _ in range(steps)]
+    t0 = time.perf_counter()
+    for s in range(steps):
+        ev[s][0].record(stream)
+        for k, f in enumerate(fns):
+            f()
+            ev[s][k + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = [float(np.mean([ev[s][k].elapsed_time(ev[s][k + 1]) for s in range(steps)])) / 1e3
+           for k in range(len(fns))]
+    gpu_total = float(np.mean([ev[s][0].elapsed_time(ev[s][-1]) for s in range(steps)])) / 1e3
+    return wall / steps, gpu_total, per
+
+
+def frac(a, p):
+    return a / p if p else None
+
+
+# ---------------------------------------------------------------------------------------
+# primary: prefix-reuse prefill step (+ first decode step) on the Llama-3-8B layer
+# ---------------------------------------------------------------------------------------
+def primary(args, lib, torch):
+    import workloads as W
+    spec = W.LLAMA3_8B_PREFILL
+    wl = Workload(spec, lib, torch)
+    b, _ = wl.batches[0]
+    dv = wl.dev[0]
+    case = wl.case
+    stream = torch.cuda.current_stream()
+    T = b.total_new
+    out = torch.empty((T, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((T, wl.hq), dtype=torch.float32, device="cuda")
+    dec = wl.decode_followup(0, lib, torch)
+    B = b.n_seqs
+    dout = torch.empty((B, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
+    dlse = torch.empty((B, wl.hq), dtype=torch.float32, device="cuda")
+    ws = lib.alloc_workspace(lib.pkv_decode_workspace_bytes(B, wl.hq, wl.hkv, wl.d,
+                                                            dec["max_len"]))
+    pk, pv = case.pool_k, case.pool_v
+
+    fns = [
+        lambda: lib.pkv_kv_append(pk, pv, b.k_new, b.v_new, dv["tables"], dv["cached"],
+                                  dv["cu"], dv["max_new"]),
+        lambda: lib.pkv_prefill_attention(pk, pv, b.q, dv["tables"], dv["cached"], dv["cu"],
+                                          dv["max_new"], dv["max_total"], wl.scale, out,
+                                          lse=lse),
+        lambda: lib.pkv_kv_append(pk, pv, dec["k"], dec["v"], dec["tables"], dec["ctx"],
+                                  dec["cu"], 1),
+        lambda: lib.pkv_decode_attention(pk, pv, dec["q"], dec["tables"], dec["seq_lens"],
+                                         dec["max_len"], wl.scale, dout, lse=dlse,
+                                         workspace=ws),
+    ]
+    step_wall, step_gpu, per = time_events(torch, stream, fns, args.steps, args.warmup)
+    t_app, t_pre, t_app1, t_dec = per
+    flops = prefill_flops(b.prefix_lens, b.new_lens, wl.hq, wl.d)
+    pbytes = prefill_bytes(b.prefix_lens, b.new_lens, wl.hq, wl.hkv, wl.d)
+    abytes = append_bytes(T, wl.hkv, wl.d)
+    dbytes = decode_bytes(dec["host_ctx"] + 1, wl.hq, wl.hkv, wl.d)
+    ms = step_wall * 1e3
+    kernels = {
+        "kv_append": {"ms": t_app * 1e3, "tokens": T, "alg_bytes": abytes,
+                      "GB_s": abytes / t_app / 1e9, "frac_hbm": abytes / t_app / 1e9 / PEAK_HBM_GBS},
+        "prefill_attention": {"ms": t_pre * 1e3, "alg_flops": flops, "alg_bytes": pbytes,
+                              "TFLOP_s": flops / t_pre / 1e12,
+                              "frac_mfma": flops / t_pre / 1e12 / PEAK_BF16_TFLOPS},
+        "kv_append_decode_token": {"ms": t_app1 * 1e3, "tokens": B,
+                                   "alg_bytes": append_bytes(B, wl.hkv, wl.d),
+                                   "note": "launch-latency bound (4 MB); no roofline claim"},
+        "decode_attention": {"ms": t_dec * 1e3, "alg_bytes": dbytes,
+                             "GB_s": dbytes / t_dec / 1e9,
+                             "frac_hbm": dbytes / t_dec / 1e9 / PEAK_HBM_GBS},
+    }
+    roof = {"bound": "mfma", "achieved": flops / t_pre / 1e12, "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s", "frac": flops / t_pre / 1e12 / PEAK_BF16_TFLOPS,
+            "traffic": traffic_from_profiles("prefill")}
+    res = {
+        "metric": METRIC,
+        "value": B / step_wall,
+        "unit": "tuples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16; no dataset)",
+        "config": {"workload": spec.name, "tuples": B, "q_heads": wl.hq, "kv_heads": wl.hkv,
+                   "head_dim": wl.d, "block_size": 16, "prefix": "U[256,1024]",
+                   "new_tokens": "U[64,256]", "new_tokens_total": T,
+                   "pool_blocks": case.num_blocks, "seed": case.seed,
+                   "step": "kv_append -> prefill_attention -> kv_append(1) -> decode_attention"},
+        "prefill_tflops": kernels["prefill_attention"]["TFLOP_s"],
+        "decode_gbps": kernels["decode_attention"]["GB_s"],
+        "tuples_per_s_gpu_time": B / step_gpu,
+        "kernels": kernels,
+        "roofline": roof,
+        "host_allocator_ms": wl.alloc_s * 1e3,
+    }
+    return res, wl, dec
+
+
+def cpu_baseline(wl, dec, budget_s=15.0):
+    """The oracle on the host cores, on a bounded sample of the same tuples: each sampled
+    tuple runs the same step (prefill of its suffix, then the first decode token)."""
+    import oracle
+    from tests.gpu_util import sub_pool_for, to_host_bits
+    try:
+        from threadpoolctl import threadpool_limits
+    except Exception:  # pragma: no cover
+        threadpool_limits = None
+    cores = len(os.sched_getaffinity(0))
+    b, _ = wl.batches[0]
+    q = to_host_bits(b.q)
+    kn, vn = to_host_bits(b.k_new), to_host_bits(b.v_new)
+    dq, dk, dvv = to_host_bits(dec["q"]), to_host_bits(dec["k"]), to_host_bits(dec["v"])
+    done, t_total = 0, 0.0
+    import contextlib
+    limit = threadpool_limits(limits=cores) if threadpool_limits else contextlib.nullcontext()
+    with limit:
+        for i in range(b.n_seqs):
+            p, n = int(b.prefix_lens[i]), int(b.new_lens[i])
+            a, e = int(b.cu_new_lens[i]), int(b.cu_new_lens[i + 1])
+            pk, pv, row = sub_pool_for(wl.case.pool_k, wl.case.pool_v, dec["host_tables"][i],
+                                       p + n + 1)
+            t0 = time.perf_counter()
+            o, _ = oracle.prefill_attention(pk, pv, row[None], [p], [0, n], q[a:e], kn[a:e],
+                                            vn[a:e], wl.scale, 16)
+            # decode: the pool now holds prefix + suffix; the oracle appends them itself
+            pk2, pv2 = oracle.kv_append(pk, pv, row[None], [p], [0, n], kn[a:e], vn[a:e], 16)
+            od, _ = oracle.decode_attention(pk2, pv2, row[None], [p + n], dq[i:i + 1],
+                                            dk[i:i + 1], dvv[i:i + 1], wl.scale, 16)
+            t_total += time.perf_counter() - t0
+            done += 1
+            if t_total >= budget_s:
+                break
+    return {"value": done / t_total, "unit": "tuples/s", "cores": cores, "kind": "oracle",
+            "sample": f"first {done} of {b.n_seqs} tuples of {wl.spec.name} (prefill of the "
+                      f"suffix + first decode token each), numpy float64, {t_total:.1f} s"}
+
+
+# ---------------------------------------------------------------------------------------
+# secondary workloads (reported beside the primary line; not the metric's workload)
+# ---------------------------------------------------------------------------------------
+def secondary(args, lib, torch):
+    import workloads as W
+    out = {}
+    stream = torch.cuda.current_stream()
+    steps, warm = max(5, args.steps // 2), 2
+
+    # paged decode, Llama-3-8B layer
+    spec = W.LLAMA3_8B_DECODE
+    wl = Workload(spec, lib, torch)
+    b, _ = wl.batches[0]
+    dv = wl.dev[0]
+    pk, pv = wl.case.pool_k, wl.case.pool_v
+    B = b.n_seqs
+    seq_lens = b.prefix_lens + 1
+    from tests.gpu_util import i32
+    sl = i32(seq_lens)
+    maxl = int(seq_lens.max())
+    o = torch.empty((B, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
+    ws = lib.alloc_workspace(lib.pkv_decode_workspace_bytes(B, wl.hq, wl.hkv, wl.d, maxl))
+    fns = [lambda: lib.pkv_kv_append(pk, pv, b.k_new, b.v_new, dv["tables"], dv["cached"],
+                                     dv["cu"], 1),
+           lambda: lib.pkv_decode_attention(pk, pv, b.q, dv["tables"], sl, maxl, wl.scale, o,
+                                            workspace=ws)]
+    _, gpu, per = time_events(torch, stream, fns, steps, warm)
+    dbytes = decode_bytes(seq_lens, wl.hq, wl.hkv, wl.d)
+    out[spec.name] = {"append_us": per[0] * 1e6, "decode_ms": per[1] * 1e3,
+                      "decode_GB_s": dbytes / per[1] / 1e9,
+                      "decode_frac_hbm": dbytes / per[1] / 1e9 / PEAK_HBM_GBS,
+                      "tuples_per_s": B / gpu}
+    del wl, pk, pv
+    torch.cuda.empty_cache()
+
+    # mixed 70B-shaped layer: append(all new tokens) -> prefill(128) -> decode(384)
+    spec = W.MIXED_70B
+    wl = Workload(spec, lib, torch)
+    (bp, _), (bd, _) = wl.batches
+    dp, dd = wl.dev
+    pk, pv = wl.case.pool_k, wl.case.pool_v
+    Tp = bp.total_new
+    op = torch.empty((Tp, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
+    od = torch.empty((bd.n_seqs, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
+    sl = i32(bd.prefix_lens + 1)
+    maxl = int(bd.prefix_lens.max()) + 1
+    ws = lib.alloc_workspace(lib.pkv_decode_workspace_bytes(bd.n_seqs, wl.hq, wl.hkv, wl.d,
+                                                            maxl))
+    fns = [lambda: lib.pkv_kv_append(pk, pv, bp.k_new, bp.v_new, dp["tables"], dp["cached"],
+                                     dp["cu"], dp["max_new"]),
+           lambda: lib.pkv_kv_append(pk, pv, bd.k_new, bd.v_new, dd["tables"], dd["cached"],
+                                     dd["cu"], 1),
+           lambda: lib.pkv_prefill_attention(pk, pv, bp.q, dp["tables"], dp["cached"],
+                                             dp["cu"], dp["max_new"], dp["max_total"],
+                                             wl.scale, op),
+           lambda: lib.pkv_decode_attention(pk, pv, bd.q, dd["tables"], sl, maxl, wl.scale,
+                                            od, workspace=ws)]
+    _, gpu, per = time_events(torch, stream, fns, steps, warm)
+    flops = prefill_flops(bp.prefix_lens, bp.new_lens, wl.hq, wl.d)
+    dbytes = decode_bytes(bd.prefix_lens + 1, wl.hq, wl.hkv, wl.d)
+    abytes = append_bytes(Tp, wl.hkv, wl.d)
+    out[spec.name] = {"append_ms": per[0] * 1e3, "append_GB_s": abytes / per[0] / 1e9,
+                      "append_decode_us": per[1] * 1e6,
+                      "prefill_ms": per[2] * 1e3, "prefill_TFLOP_s": flops / per[2] / 1e12,
+                      "prefill_frac_mfma": flops / per[2] / 1e12 / PEAK_BF16_TFLOPS,
+                      "decode_ms": per[3] * 1e3, "decode_GB_s": dbytes / per[3] / 1e9,
+                      "decode_frac_hbm": dbytes / per[3] / 1e9 / PEAK_HBM_GBS,
+                      "set_ms": gpu * 1e3, "sequences_per_s": (bp.n_seqs + bd.n_seqs) / gpu}
+    del wl, pk, pv
+    torch.cuda.empty_cache()
+
+    # long documents with a shared 512-token prompt
+    spec = W.LONG_DOC_SHARED_PROMPT
+    wl = Workload(spec, lib, torch)
+    b, _ = wl.batches[0]
+    dv = wl.dev[0]
+    pk, pv = wl.case.pool_k, wl.case.pool_v
+    o = torch.empty((b.total_new, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
+    fns = [lambda: lib.pkv_kv_append(pk, pv, b.k_new, b.v_new, dv["tables"], dv["cached"],
+                                     dv["cu"], dv["max_new"]),
+           lambda: lib.pkv_prefill_attention(pk, pv, b.q, dv["tables"], dv["cached"], dv["cu"],
+                                             dv["max_new"], dv["max_total"], wl.scale, o)]
+    _, gpu, per = time_events(torch, stream, fns, steps, warm)
+    flops = prefill_flops(b.prefix_lens, b.new_lens, wl.hq, wl.d)
+    abytes = append_bytes(b.total_new, wl.hkv, wl.d)
+    out[spec.name] = {"append_ms": per[0] * 1e3, "append_GB_s": abytes / per[0] / 1e9,
+                      "prefill_ms": per[1] * 1e3, "prefill_TFLOP_s": flops / per[1] / 1e12,
+                      "prefill_frac_mfma": flops / per[1] / 1e12 / PEAK_BF16_TFLOPS,
+                      "tuples_per_s": b.n_seqs / gpu}
+    del wl, pk, pv
+    torch.cuda.empty_cache()
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this path needs no collective and runs one "
+              "process on one MI355X (see DESIGN.md for how it would shard).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    from paper_2607_23815_amd import lib
+    log(f"[bench] primary workload, steps={args.steps} warmup={args.warmup}")
+    res, wl, dec = primary(args, lib, torch)
+    log(f"[bench] primary done: {res['ms_per_step']:.3f} ms/step")
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle) ...")
+        res["cpu_baseline"] = cpu_baseline(wl, dec)
+        log("[bench] cpu baseline done")
+    else:
+        res["cpu_baseline"] = None
+    del wl, dec
+    torch.cuda.empty_cache()
+    if not args.no_secondary:
+        log("[bench] secondary workloads ...")
+        res["secondary"] = secondary(args, lib, torch)
+        log("[bench] secondary done")
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,198 @@
+/*
+ * pkv.h -- paged prefix-reuse attention for MI355X (gfx950): the C ABI.
+ *
+ * The library keeps a pool of fixed-size KV blocks addressed through per-sequence block
+ * tables, appends new tokens' K/V into it, and runs attention over it for two phases:
+ *   - a downstream operator's prefill, which reuses the KV cache a tuple's cached prompt
+ *     prefix already holds and computes only the new suffix tokens, and
+ *   - decode, one new token per sequence attending over the whole cached context.
+ * This is the KV-cache reuse that pipelining semantic operators relies on: the filter -> map
+ * example of Section 2.1 ("Prefix sharing in semantic operators") has prompts
+ * [S | C(t) | I_filter] and [S | C(t) | I_map] whose shared prefix [S | C(t)] is cached once
+ * and reused, so the map "only prefills the map-specific suffix". The block pool follows the
+ * "vLLM memory model" paragraph of Section 2.1 (fixed-size blocks like virtual-memory pages,
+ * taken on admission, returned on completion, requests deferred when blocks run out).
+ *
+ * Conventions
+ *   - Every call returns pkv_status. On failure pkv_last_error() gives a message (thread-
+ *     local, valid until this thread's next pkv call). Argument checks happen on the host
+ *     before any launch; a failed call has launched nothing and changed no state.
+ *   - Supported shapes: block_size 16; head_dim 64 or 128; num_q_heads a multiple of
+ *     num_kv_heads; decode additionally needs num_q_heads / num_kv_heads <= 16. Anything else
+ *     returns PKV_ERR_UNSUPPORTED_SHAPE. Zero sequences or zero tokens is a successful no-op.
+ *   - Device calls take device pointers (caller-owned; the library never allocates or frees
+ *     device memory) and a hipStream_t passed as void* (NULL = the null stream). They are
+ *     asynchronous; results are ready when the stream has drained. A launch failure returns
+ *     PKV_ERR_HIP with hipGetErrorString's text. Device calls are reentrant.
+ *   - The contents of device metadata (block ids within the pool, lengths within the table)
+ *     are the caller's contract: the host cannot check them without a device-to-host copy.
+ *     Every kernel bounds the table index it computes by max_blocks and skips -1 entries.
+ *   - bf16 is IEEE binary16 "brain float" (1 sign, 8 exponent, 7 mantissa bits), stored as
+ *     16-bit words.
+ *
+ * KV pool layout (one attention layer; caller-allocated, 256-byte aligned):
+ *   K cache: bf16 [num_blocks][num_kv_heads][head_dim/8][block_size][8]
+ *            dim d of the token in slot s is element [.., d/8, s, d%8]: a block's slab for one
+ *            kv head is head_dim/8 runs of block_size 16-byte chunks.
+ *   V cache: bf16 [num_blocks][num_kv_heads][head_dim][block_size]
+ *            dim d of slot s is element [.., d, s]: the slab is stored dim-major.
+ *   Logical token t of a sequence lives in block block_tables[seq][t / block_size], slot
+ *   t % block_size. Both layouts let attention feed the matrix cores straight from 16-byte
+ *   loads (K rows for the score product, V columns for the value product).
+ */
+#ifndef PKV_H
+#define PKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PKV_OK = 0,
+  PKV_ERR_INVALID_ARG = 1,        /* null pointer, negative size, inconsistent sizes */
+  PKV_ERR_OUT_OF_BLOCKS = 2,      /* reserve refused: too few free blocks; nothing changed */
+  PKV_ERR_SHARED_BLOCK_WRITE = 3, /* reserve refused: the write range hits a shared block */
+  PKV_ERR_UNSUPPORTED_SHAPE = 4,  /* block_size / head_dim / head ratio not supported */
+  PKV_ERR_NOT_FOUND = 5,          /* unknown sequence id */
+  PKV_ERR_HIP = 6                 /* a HIP runtime call or launch failed */
+} pkv_status;
+
+/* Message of this thread's last failed call ("" if none). */
+const char* pkv_last_error(void);
+
+/* ABI version, bumped on any incompatible change. */
+int32_t pkv_abi_version(void);
+
+/* ---------------------------------------------------------------------------------------
+ * Block pool: host-side bookkeeping of which physical blocks each sequence (tuple) holds.
+ * Section 2.1 ("vLLM memory model"): a global pool of fixed-size blocks, taken when a
+ * request is admitted and returned when it completes; when blocks run short the request is
+ * deferred. Section 4 (predicate contract): a dropped tuple frees its prefix. Section 5.3
+ * (Algorithm 1, Complete): a parent's memory is released only after all its children.
+ * A pool is not thread-safe; distinct pools are independent. It owns no device memory.
+ * --------------------------------------------------------------------------------------- */
+typedef struct pkv_pool pkv_pool;
+
+/* Create a pool of num_blocks blocks of block_size tokens. free_order (host, may be NULL):
+ * the order in which blocks are handed out, a permutation of 0..num_blocks-1 (NULL means
+ * ascending); a seeded permutation gives the random block placement of a fragmented pool.
+ * The array is copied. *out receives the pool. */
+pkv_status pkv_pool_create(int32_t num_blocks, int32_t block_size, const int32_t* free_order,
+                           pkv_pool** out);
+void pkv_pool_destroy(pkv_pool* pool);
+int32_t pkv_pool_num_free(const pkv_pool* pool);  /* -1 for a NULL pool */
+
+/* New empty sequence; ids start at 1 and are never reused within a pool. */
+pkv_status pkv_seq_create(pkv_pool* pool, int64_t* seq_id);
+
+/* New sequence sharing the first shared_tokens tokens of parent (a multiple of block_size,
+ * at most the parent's committed length) by reference: the shared blocks' reference counts
+ * go up, and they return to the free list only when every holder has been freed. */
+pkv_status pkv_seq_fork(pkv_pool* pool, int64_t parent, int32_t shared_tokens, int64_t* child);
+
+/* Reserve room for new_tokens more tokens after the sequence's committed and already
+ * reserved tokens. All-or-nothing: OUT_OF_BLOCKS when too few blocks are free and
+ * SHARED_BLOCK_WRITE when the range would write into a block held by another sequence; in
+ * both cases nothing changes. Blocks come from the front of the free list, in order. */
+pkv_status pkv_seq_reserve(pkv_pool* pool, int64_t seq, int32_t new_tokens);
+
+/* Mark new_tokens reserved tokens as written (after kv_append); 0 <= new_tokens <= reserved. */
+pkv_status pkv_seq_commit(pkv_pool* pool, int64_t seq, int32_t new_tokens);
+
+/* Drop a sequence: each of its blocks loses one reference; a block whose count reaches zero
+ * goes to the back of the free list (in table order). */
+pkv_status pkv_seq_free(pkv_pool* pool, int64_t seq);
+
+/* Committed length of a sequence. */
+pkv_status pkv_seq_len(const pkv_pool* pool, int64_t seq, int32_t* len);
+
+/* Export block tables: host_tables [n][max_blocks] receives each sequence's physical block
+ * ids (reserved blocks included), padded with -1; host_lens [n] (may be NULL) receives the
+ * committed lengths, i.e. the cached_lens of a following append/prefill. INVALID_ARG if a
+ * sequence holds more than max_blocks blocks. Nothing is written on failure. */
+pkv_status pkv_fill_block_tables(const pkv_pool* pool, const int64_t* seq_ids, int32_t n,
+                                 int32_t max_blocks, int32_t* host_tables, int32_t* host_lens);
+
+/* ---------------------------------------------------------------------------------------
+ * Device calls.
+ * --------------------------------------------------------------------------------------- */
+typedef struct {
+  void* k_cache;        /* bf16, layout above */
+  void* v_cache;        /* bf16, layout above */
+  int32_t num_blocks;
+  int32_t block_size;   /* 16 */
+  int32_t num_kv_heads;
+  int32_t head_dim;     /* 64 or 128 */
+} pkv_paged_kv;
+
+/* KV append / scatter. Prefill materialises per-layer K/V for the prompt tokens and decode
+ * adds one token at a time (Section 2.1, "Background"); a downstream operator extends the
+ * tuple's cached prefix with its own suffix. For each sequence i < num_seqs and each new
+ * token j < N_i = cu_new_lens[i+1] - cu_new_lens[i], row cu_new_lens[i] + j of k_new / v_new
+ * (bf16 [total_new][num_kv_heads][head_dim], row-major) is copied bit-exactly into logical
+ * position cached_lens[i] + j of sequence i. No other byte of the pool is modified (a
+ * partially covered 16-byte V chunk is read and written back unchanged outside the new
+ * slots). block_tables: int32 [num_seqs][max_blocks]; cached_lens: int32 [num_seqs];
+ * cu_new_lens: int32 [num_seqs + 1], cu_new_lens[0] = 0, non-decreasing,
+ * cu_new_lens[num_seqs] = total_new. max_new_len (host) >= every N_i sizes the grid. The
+ * target blocks must be private to the sequence (the allocator guarantees this). */
+pkv_status pkv_kv_append(const pkv_paged_kv* kv, const void* k_new, const void* v_new,
+                         const int32_t* block_tables, int32_t max_blocks,
+                         const int32_t* cached_lens, const int32_t* cu_new_lens,
+                         int32_t num_seqs, int32_t total_new, int32_t max_new_len,
+                         void* stream);
+
+/* Prefix-reuse prefill attention. Section 2.1: the cached prefix's KV is reused and only the
+ * suffix is computed. For sequence i with P_i = cached_lens[i] cached tokens and N_i new
+ * tokens (already appended at positions P_i .. P_i + N_i - 1), new token j and query head h
+ * attend over keys 0 .. P_i + j of kv head h / (num_q_heads / num_kv_heads):
+ *   out[r][h] = sum_t softmax_t(scale * <q[r][h], K[t]>) V[t],   r = cu_new_lens[i] + j,
+ * and lse[r][h] = ln sum_t exp(scale * <q[r][h], K[t]>). These are rows P_i.. of causal
+ * attention over the whole P_i + N_i tokens. q, out: bf16 [total_new][num_q_heads][head_dim];
+ * lse: float [total_new][num_q_heads] or NULL. bf16 inputs, fp32 accumulation, bf16 output
+ * (round to nearest even). max_new_len (host) >= every N_i; max_total_len (host) >= every
+ * P_i + N_i. workspace may be NULL when pkv_prefill_workspace_bytes returns 0. */
+pkv_status pkv_prefill_attention(const pkv_paged_kv* kv, const void* q, int32_t num_q_heads,
+                                 const int32_t* block_tables, int32_t max_blocks,
+                                 const int32_t* cached_lens, const int32_t* cu_new_lens,
+                                 int32_t num_seqs, int32_t total_new, int32_t max_new_len,
+                                 int32_t max_total_len, float scale, void* out, float* lse,
+                                 void* workspace, size_t workspace_bytes, void* stream);
+size_t pkv_prefill_workspace_bytes(int32_t num_seqs, int32_t total_new, int32_t num_q_heads,
+                                   int32_t num_kv_heads, int32_t head_dim,
+                                   int32_t max_new_len, int32_t max_total_len);
+
+/* Paged decode attention (Section 2.1: decode generates one token at a time, attending over
+ * all previously computed K/V). Sequence i's single query q[i] attends over all
+ * seq_lens[i] keys (the cached context plus the token this step appended):
+ *   out[i][h] = sum_{t < seq_lens[i]} softmax_t(scale * <q[i][h], K[t]>) V[t].
+ * The key range is cut into splits whose boundaries depend only on key positions; each split
+ * writes a partial result to the workspace and a second kernel merges them with their
+ * log-sum-exp weights. q, out: bf16 [num_seqs][num_q_heads][head_dim]; lse: float
+ * [num_seqs][num_q_heads] or NULL; seq_lens: int32 [num_seqs], each >= 1. max_seq_len (host)
+ * >= every seq_lens[i]. workspace: device memory of at least pkv_decode_workspace_bytes. */
+pkv_status pkv_decode_attention(const pkv_paged_kv* kv, const void* q, int32_t num_q_heads,
+                                const int32_t* block_tables, int32_t max_blocks,
+                                const int32_t* seq_lens, int32_t num_seqs, int32_t max_seq_len,
+                                float scale, void* out, float* lse, void* workspace,
+                                size_t workspace_bytes, void* stream);
+size_t pkv_decode_workspace_bytes(int32_t num_seqs, int32_t num_q_heads, int32_t num_kv_heads,
+                                  int32_t head_dim, int32_t max_seq_len);
+
+/* Paged gather (test support): copies the first lens[i] tokens of every sequence out of the
+ * pool into contiguous k_out / v_out, bf16 [sum lens][num_kv_heads][head_dim], sequence i
+ * starting at row cu_lens[i] (int32 [num_seqs + 1]). Bit-exact. max_len (host) >= every
+ * lens[i]. */
+pkv_status pkv_gather_kv(const pkv_paged_kv* kv, const int32_t* block_tables,
+                         int32_t max_blocks, const int32_t* lens, const int32_t* cu_lens,
+                         int32_t num_seqs, int32_t max_len, void* k_out, void* v_out,
+                         void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PKV_H */

@@ -1,0 +1,219 @@
+// The C ABI's device calls: host-side argument validation, then the gfx950 kernel launches.
+// Every check happens before any launch, so a refused call has enqueued nothing.
+#include <hip/hip_runtime.h>
+
+#include <string>
+
+#include "internal.h"
+#include "launch.h"
+
+namespace pkv {
+
+namespace {
+thread_local std::string g_last_error;
+}
+
+pkv_status fail(pkv_status status, const std::string& message) {
+  g_last_error = message;
+  return status;
+}
+
+pkv_status ok() {
+  g_last_error.clear();
+  return PKV_OK;
+}
+
+namespace {
+
+constexpr int kMaxGridZ = 65535;
+
+pkv_status check_kv(const pkv_paged_kv* kv, const char* fn, KvView* view) {
+  const std::string f(fn);
+  if (kv == nullptr) return fail(PKV_ERR_INVALID_ARG, f + ": kv is NULL");
+  if (kv->k_cache == nullptr || kv->v_cache == nullptr)
+    return fail(PKV_ERR_INVALID_ARG, f + ": k_cache / v_cache is NULL");
+  if (kv->num_blocks <= 0 || kv->num_kv_heads <= 0)
+    return fail(PKV_ERR_INVALID_ARG, f + ": num_blocks and num_kv_heads must be positive");
+  if (kv->block_size != kSupportedBlockSize)
+    return fail(PKV_ERR_UNSUPPORTED_SHAPE, f + ": block_size must be 16");
+  if (kv->head_dim != 64 && kv->head_dim != 128)
+    return fail(PKV_ERR_UNSUPPORTED_SHAPE, f + ": head_dim must be 64 or 128");
+  if ((reinterpret_cast<uintptr_t>(kv->k_cache) | reinterpret_cast<uintptr_t>(kv->v_cache)) & 15)
+    return fail(PKV_ERR_INVALID_ARG, f + ": k_cache / v_cache must be 16-byte aligned");
+  view->k = static_cast<uint16_t*>(kv->k_cache);
+  view->v = static_cast<uint16_t*>(kv->v_cache);
+  view->num_blocks = kv->num_blocks;
+  view->hkv = kv->num_kv_heads;
+  view->head_dim = kv->head_dim;
+  return PKV_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+pkv_status launched(hipError_t err, const char* fn) {
+  if (err != hipSuccess)
+    return fail(PKV_ERR_HIP, std::string(fn) + ": " + hipGetErrorString(err));
+  return ok();
+}
+
+}  // namespace
+}  // namespace pkv
+
+using namespace pkv;
+
+extern "C" {
+
+const char* pkv_last_error(void) { return pkv::g_last_error.c_str(); }
+
+int32_t pkv_abi_version(void) { return 1; }
+
+pkv_status pkv_kv_append(const pkv_paged_kv* kv, const void* k_new, const void* v_new,
+                         const int32_t* block_tables, int32_t max_blocks,
+                         const int32_t* cached_lens, const int32_t* cu_new_lens,
+                         int32_t num_seqs, int32_t total_new, int32_t max_new_len,
+                         void* stream) {
+  const char* fn = "pkv_kv_append";
+  KvView view;
+  pkv_status st = check_kv(kv, fn, &view);
+  if (st != PKV_OK) return st;
+  if (num_seqs < 0 || total_new < 0 || max_new_len < 0 || max_blocks < 0)
+    return fail(PKV_ERR_INVALID_ARG, "pkv_kv_append: negative size");
+  if (num_seqs == 0 || total_new == 0) return ok();
+  if (k_new == nullptr || v_new == nullptr || block_tables == nullptr ||
+      cached_lens == nullptr || cu_new_lens == nullptr)
+    return fail(PKV_ERR_INVALID_ARG, "pkv_kv_append: NULL pointer");
+  if (!aligned16(k_new) || !aligned16(v_new))
+    return fail(PKV_ERR_INVALID_ARG, "pkv_kv_append: k_new / v_new must be 16-byte aligned");
+  if (max_new_len == 0 || max_blocks == 0)
+    return fail(PKV_ERR_INVALID_ARG, "pkv_kv_append: max_new_len and max_blocks must be > 0");
+  if (num_seqs > kMaxGridZ)
+    return fail(PKV_ERR_INVALID_ARG, "pkv_kv_append: more than 65535 sequences per call");
+  return launched(launch_kv_append(view, static_cast<const uint16_t*>(k_new),
+                                   static_cast<const uint16_t*>(v_new), block_tables,
+                                   max_blocks, cached_lens, cu_new_lens, num_seqs, max_new_len,
+                                   static_cast<hipStream_t>(stream)),
+                  fn);
+}
+
+size_t pkv_prefill_workspace_bytes(int32_t num_seqs, int32_t total_new, int32_t num_q_heads,
+                                   int32_t num_kv_heads, int32_t head_dim, int32_t max_new_len,
+                                   int32_t max_total_len) {
+  (void)num_seqs; (void)total_new; (void)num_q_heads; (void)num_kv_heads; (void)head_dim;
+  (void)max_new_len; (void)max_total_len;
+  return 0;
+}
+
+pkv_status pkv_prefill_attention(const pkv_paged_kv* kv, const void* q, int32_t num_q_heads,
+                                 const int32_t* block_tables, int32_t max_blocks,
+                                 const int32_t* cached_lens, const int32_t* cu_new_lens,
+                                 int32_t num_seqs, int32_t total_new, int32_t max_new_len,
+                                 int32_t max_total_len, float scale, void* out, float* lse,
+                                 void* workspace, size_t workspace_bytes, void* stream) {
+  const char* fn = "pkv_prefill_attention";
+  KvView view;
+  pkv_status st = check_kv(kv, fn, &view);
+  if (st != PKV_OK) return st;
+  if (num_q_heads <= 0 || num_q_heads % view.hkv != 0)
+    return fail(PKV_ERR_UNSUPPORTED_SHAPE,
+                "pkv_prefill_attention: num_q_heads must be a positive multiple of num_kv_heads");
+  if (num_seqs < 0 || total_new < 0 || max_new_len < 0 || max_total_len < 0 || max_blocks < 0)
+    return fail(PKV_ERR_INVALID_ARG, "pkv_prefill_attention: negative size");
+  if (num_seqs == 0 || total_new == 0) return ok();
+  if (q == nullptr || out == nullptr || block_tables == nullptr || cached_lens == nullptr ||
+      cu_new_lens == nullptr)
+    return fail(PKV_ERR_INVALID_ARG, "pkv_prefill_attention: NULL pointer");
+  if (!aligned16(q) || !aligned16(out))
+    return fail(PKV_ERR_INVALID_ARG, "pkv_prefill_attention: q / out must be 16-byte aligned");
+  if (max_new_len == 0 || max_total_len < max_new_len || max_blocks == 0)
+    return fail(PKV_ERR_INVALID_ARG,
+                "pkv_prefill_attention: need 0 < max_new_len <= max_total_len, max_blocks > 0");
+  if ((int64_t)max_blocks * kSupportedBlockSize < max_total_len)
+    return fail(PKV_ERR_INVALID_ARG,
+                "pkv_prefill_attention: max_total_len exceeds max_blocks * block_size");
+  if (!(scale > 0.f)) return fail(PKV_ERR_INVALID_ARG, "pkv_prefill_attention: scale <= 0");
+  if (num_seqs > kMaxGridZ)
+    return fail(PKV_ERR_INVALID_ARG, "pkv_prefill_attention: more than 65535 sequences");
+  const size_t need = pkv_prefill_workspace_bytes(num_seqs, total_new, num_q_heads, view.hkv,
+                                                  view.head_dim, max_new_len, max_total_len);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need))
+    return fail(PKV_ERR_INVALID_ARG, "pkv_prefill_attention: workspace too small");
+  return launched(launch_prefill(view, static_cast<const uint16_t*>(q), num_q_heads,
+                                 block_tables, max_blocks, cached_lens, cu_new_lens, num_seqs,
+                                 max_new_len, scale, static_cast<uint16_t*>(out), lse,
+                                 static_cast<hipStream_t>(stream)),
+                  fn);
+}
+
+size_t pkv_decode_workspace_bytes(int32_t num_seqs, int32_t num_q_heads, int32_t num_kv_heads,
+                                  int32_t head_dim, int32_t max_seq_len) {
+  if (num_seqs <= 0 || num_q_heads <= 0 || num_kv_heads <= 0 || head_dim <= 0 ||
+      max_seq_len <= 0)
+    return 0;
+  return decode_workspace_bytes(num_seqs, num_q_heads, num_kv_heads, head_dim, max_seq_len);
+}
+
+pkv_status pkv_decode_attention(const pkv_paged_kv* kv, const void* q, int32_t num_q_heads,
+                                const int32_t* block_tables, int32_t max_blocks,
+                                const int32_t* seq_lens, int32_t num_seqs, int32_t max_seq_len,
+                                float scale, void* out, float* lse, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  const char* fn = "pkv_decode_attention";
+  KvView view;
+  pkv_status st = check_kv(kv, fn, &view);
+  if (st != PKV_OK) return st;
+  if (num_q_heads <= 0 || num_q_heads % view.hkv != 0 || num_q_heads / view.hkv > 16)
+    return fail(PKV_ERR_UNSUPPORTED_SHAPE,
+                "pkv_decode_attention: num_q_heads must be a multiple of num_kv_heads, with "
+                "at most 16 query heads per kv head");
+  if (num_seqs < 0 || max_seq_len < 0 || max_blocks < 0)
+    return fail(PKV_ERR_INVALID_ARG, "pkv_decode_attention: negative size");
+  if (num_seqs == 0) return ok();
+  if (q == nullptr || out == nullptr || block_tables == nullptr || seq_lens == nullptr)
+    return fail(PKV_ERR_INVALID_ARG, "pkv_decode_attention: NULL pointer");
+  if (!aligned16(q) || !aligned16(out))
+    return fail(PKV_ERR_INVALID_ARG, "pkv_decode_attention: q / out must be 16-byte aligned");
+  if (max_seq_len == 0 || max_blocks == 0)
+    return fail(PKV_ERR_INVALID_ARG, "pkv_decode_attention: max_seq_len, max_blocks must be > 0");
+  if ((int64_t)max_blocks * kSupportedBlockSize < max_seq_len)
+    return fail(PKV_ERR_INVALID_ARG,
+                "pkv_decode_attention: max_seq_len exceeds max_blocks * block_size");
+  if (!(scale > 0.f)) return fail(PKV_ERR_INVALID_ARG, "pkv_decode_attention: scale <= 0");
+  const size_t need = decode_workspace_bytes(num_seqs, num_q_heads, view.hkv, view.head_dim,
+                                             max_seq_len);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need || !aligned16(workspace)))
+    return fail(PKV_ERR_INVALID_ARG,
+                "pkv_decode_attention: workspace missing, too small or not 16-byte aligned "
+                "(see pkv_decode_workspace_bytes)");
+  return launched(launch_decode(view, static_cast<const uint16_t*>(q), num_q_heads,
+                                block_tables, max_blocks, seq_lens, num_seqs, max_seq_len, scale,
+                                static_cast<uint16_t*>(out), lse, workspace,
+                                static_cast<hipStream_t>(stream)),
+                  fn);
+}
+
+pkv_status pkv_gather_kv(const pkv_paged_kv* kv, const int32_t* block_tables,
+                         int32_t max_blocks, const int32_t* lens, const int32_t* cu_lens,
+                         int32_t num_seqs, int32_t max_len, void* k_out, void* v_out,
+                         void* stream) {
+  const char* fn = "pkv_gather_kv";
+  KvView view;
+  pkv_status st = check_kv(kv, fn, &view);
+  if (st != PKV_OK) return st;
+  if (num_seqs < 0 || max_len < 0 || max_blocks < 0)
+    return fail(PKV_ERR_INVALID_ARG, "pkv_gather_kv: negative size");
+  if (num_seqs == 0 || max_len == 0) return ok();
+  if (block_tables == nullptr || lens == nullptr || cu_lens == nullptr || k_out == nullptr ||
+      v_out == nullptr)
+    return fail(PKV_ERR_INVALID_ARG, "pkv_gather_kv: NULL pointer");
+  if (!aligned16(k_out) || !aligned16(v_out))
+    return fail(PKV_ERR_INVALID_ARG, "pkv_gather_kv: outputs must be 16-byte aligned");
+  if (num_seqs > kMaxGridZ)
+    return fail(PKV_ERR_INVALID_ARG, "pkv_gather_kv: more than 65535 sequences per call");
+  return launched(launch_gather_kv(view, block_tables, max_blocks, lens, cu_lens, num_seqs,
+                                   max_len, static_cast<uint16_t*>(k_out),
+                                   static_cast<uint16_t*>(v_out),
+                                   static_cast<hipStream_t>(stream)),
+                  fn);
+}
+
+}  // extern "C"

@@ -1,0 +1,297 @@
+// Paged decode attention for gfx950: one query token per sequence over its whole cached
+// context, split along the key axis ("split-K") so that every compute unit streams KV at the
+// HBM rate, followed by a merge of the splits' partial results by their log-sum-exp weights.
+//
+// Work item = (sequence, kv head, split) = one wavefront; a 256-thread workgroup carries four
+// independent work items, so there are no barriers and no LDS. Each wave streams its split
+// 32 keys (two 16-token blocks) at a time straight from HBM into the matrix-core operands:
+//   scores  S^T[32 keys][16 cols] = K[keys][D] . Q^T[D][cols]      (v_mfma 16x16x32 bf16)
+//   values  O^T[D][16 cols]      += V^T[D][32 keys] . P^T[keys][cols]
+// The columns are the g = Hq/Hkv query heads that share the kv head (g <= 16; unused columns
+// carry zero queries), so every KV byte is read once per kv head, never once per query head.
+// Both products take 16-byte K loads and 8-byte V loads that are contiguous across the wave:
+// the K pool slab is chunk-major ([D/8][16 slots][8]), so lane (slot s, chunk group q) of
+// load kk reads chunk q + 4kk of slot s and one instruction covers 1 KB contiguous; the V pool
+// slab is dim-major ([D][16 slots]), so lanes read 4 consecutive slots of one dim.
+// The online softmax runs in the base-2 domain (scale * log2 e folded in fp32); per-column
+// max and sum are combined across the four lane groups holding a column with cross-lane
+// shuffles. Keys outside the sequence (tail slots of its last block, which may hold any bits,
+// NaN included) are removed by selection -- scores to -inf and V operands to zero -- never by
+// multiplying by a zero weight.
+// Split boundaries are multiples of the split size in key position only, so results are
+// bit-identical from run to run and independent of where blocks sit in the pool.
+#include <math.h>
+
+#include "device_utils.h"
+#include "launch.h"
+
+namespace pkv {
+namespace {
+
+constexpr int kWaves = 4;
+
+__device__ __forceinline__ float wave_max16(float x) {
+  // max over the four lanes l, l^16, l^32, l^48 (the lane groups holding one column)
+  x = fmaxf(x, __shfl_xor(x, 16));
+  x = fmaxf(x, __shfl_xor(x, 32));
+  return x;
+}
+__device__ __forceinline__ float wave_sum16(float x) {
+  x += __shfl_xor(x, 16);
+  x += __shfl_xor(x, 32);
+  return x;
+}
+
+// zero the 16-bit lanes of a 4-element V fragment whose key index (base + e) >= nvalid
+__device__ __forceinline__ u32x2 mask_v4(u32x2 v, int base, int nvalid) {
+  uint32_t w0 = v[0], w1 = v[1];
+  if (base + 0 >= nvalid) w0 &= 0xFFFF0000u;
+  if (base + 1 >= nvalid) w0 &= 0x0000FFFFu;
+  if (base + 2 >= nvalid) w1 &= 0xFFFF0000u;
+  if (base + 3 >= nvalid) w1 &= 0x0000FFFFu;
+  u32x2 r = {w0, w1};
+  return r;
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void decode_partial_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
+    const uint16_t* __restrict__ v_cache, const int32_t* __restrict__ block_tables,
+    int32_t max_blocks, const int32_t* __restrict__ seq_lens, int32_t num_seqs, int32_t hq,
+    int32_t hkv, int32_t num_blocks, int32_t split_keys, int32_t max_splits, float scale_log2,
+    float* __restrict__ ws_o, float* __restrict__ ws_ml, uint16_t* __restrict__ out,
+    float* __restrict__ lse) {
+  constexpr int KK = D / 32;   // k-steps of the score product
+  constexpr int DB = D / 16;   // 16-dim blocks of the value product
+  constexpr int SLAB = D * kBlockSize;
+  const int g = hq / hkv;
+  const int lane = threadIdx.x & 63;
+  const int col = lane & 15;   // query head within the kv group (column)
+  const int grp = lane >> 4;   // lane group 0..3
+  const int64_t item = (int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6);
+  const int64_t per_seq = (int64_t)hkv * max_splits;
+  const int i = (int)(item / per_seq);
+  if (i >= num_seqs) return;
+  const int rem = (int)(item % per_seq);
+  const int kvh = rem / max_splits;
+  const int sp = rem % max_splits;
+  const int len = seq_lens[i];
+  const int nsplit = (len + split_keys - 1) / split_keys;
+  if (sp >= nsplit) return;
+  const int k0 = sp * split_keys;
+  const int k1 = min(len, k0 + split_keys);
+  const bool col_ok = col < g;
+  const int h = kvh * g + col;
+
+  bf16x8 qf[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (col_ok) v = ld16(q + ((size_t)i * hq + h) * D + kk * 32 + grp * 8);
+    qf[kk] = as_bf16x8(v);
+  }
+
+  f32x4 acc[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m = -INFINITY;
+  float lpart = 0.f;
+  const int32_t* table = block_tables + (size_t)i * max_blocks;
+  const size_t head_off = (size_t)kvh * SLAB;
+
+  for (int t0 = k0; t0 < k1; t0 += 32) {
+    const int nvalid = min(32, k1 - t0);
+    const int b0 = t0 / kBlockSize;
+    int blk0 = (b0 < max_blocks) ? table[b0] : -1;
+    int blk1 = (nvalid > kBlockSize && b0 + 1 < max_blocks) ? table[b0 + 1] : -1;
+    if (blk0 >= num_blocks) blk0 = -1;
+    if (blk1 >= num_blocks) blk1 = -1;
+    const uint16_t* k0p = k_cache + (size_t)max(blk0, 0) * hkv * SLAB + head_off;
+    const uint16_t* k1p = k_cache + (size_t)max(blk1, 0) * hkv * SLAB + head_off;
+    const uint16_t* v0p = v_cache + (size_t)max(blk0, 0) * hkv * SLAB + head_off;
+    const uint16_t* v1p = v_cache + (size_t)max(blk1, 0) * hkv * SLAB + head_off;
+
+    // scores for the two blocks
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      const int chunk = grp + 4 * kk;
+      u32x4 a0 = {0u, 0u, 0u, 0u}, a1 = {0u, 0u, 0u, 0u};
+      if (blk0 >= 0) a0 = ld16(k0p + (size_t)(chunk * kBlockSize + col) * 8);
+      if (blk1 >= 0) a1 = ld16(k1p + (size_t)(chunk * kBlockSize + col) * 8);
+      s0 = mfma16(as_bf16x8(a0), qf[kk], s0);
+      s1 = mfma16(as_bf16x8(a1), qf[kk], s1);
+    }
+    // lane holds keys 4*grp + r (block 0) and 16 + 4*grp + r (block 1) of column col
+    float sv[8];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      sv[r] = (4 * grp + r < nvalid && blk0 >= 0) ? s0[r] * scale_log2 : -INFINITY;
+      sv[4 + r] = (16 + 4 * grp + r < nvalid && blk1 >= 0) ? s1[r] * scale_log2 : -INFINITY;
+    }
+    float mx = sv[0];
+#pragma unroll
+    for (int r = 1; r < 8; ++r) mx = fmaxf(mx, sv[r]);
+    mx = wave_max16(mx);
+    const float m_new = fmaxf(m, mx);
+    const float alpha = fast_exp2(m - m_new);
+    float pv[8];
+    float ps = 0.f;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      pv[r] = fast_exp2(sv[r] - m_new);
+      ps += pv[r];
+    }
+    lpart = lpart * alpha + ps;
+    m = m_new;
+    u32x4 pb;
+    pb[0] = pack_bf16x2(pv[0], pv[1]);
+    pb[1] = pack_bf16x2(pv[2], pv[3]);
+    pb[2] = pack_bf16x2(pv[4], pv[5]);
+    pb[3] = pack_bf16x2(pv[6], pv[7]);
+    const bf16x8 pfrag = as_bf16x8(pb);
+
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int d = db * 16 + col;
+      u32x2 va = {0u, 0u}, vb = {0u, 0u};
+      if (blk0 >= 0) va = ld8(v0p + (size_t)d * kBlockSize + 4 * grp);
+      if (blk1 >= 0) vb = ld8(v1p + (size_t)d * kBlockSize + 4 * grp);
+      if (nvalid < 32) {
+        va = mask_v4(va, 4 * grp, nvalid);
+        vb = mask_v4(vb, 16 + 4 * grp, nvalid);
+      }
+      u32x4 vv = {va[0], va[1], vb[0], vb[1]};
+      f32x4 c = acc[db];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) c[r] *= alpha;
+      acc[db] = mfma16(as_bf16x8(vv), pfrag, c);
+    }
+  }
+
+  const float l = wave_sum16(lpart);
+  if (!col_ok) return;
+  if (nsplit == 1) {
+    const float inv = 1.f / l;
+    uint16_t* o = out + ((size_t)i * hq + h) * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      u32x2 w = {pack_bf16x2(acc[db][0] * inv, acc[db][1] * inv),
+                 pack_bf16x2(acc[db][2] * inv, acc[db][3] * inv)};
+      st8(o + db * 16 + 4 * grp, w);
+    }
+    if (lse != nullptr && grp == 0) lse[(size_t)i * hq + h] = (m + log2f(l)) * kLn2;
+    return;
+  }
+  const size_t slot = ((size_t)i * hq + h) * max_splits + sp;
+  float* o = ws_o + slot * D;
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    f32x4 c = acc[db];
+    st16(o + db * 16 + 4 * grp, __builtin_bit_cast(u32x4, c));
+  }
+  if (grp == 0) {
+    ws_ml[slot * 2 + 0] = m;
+    ws_ml[slot * 2 + 1] = l;
+  }
+}
+
+// One wave per (sequence, query head): combine the splits' partial (m_s, l_s, acc_s):
+//   out = sum_s 2^(m_s - M) acc_s / sum_s 2^(m_s - M) l_s,   M = max_s m_s.
+template <int D>
+__global__ __launch_bounds__(256) void decode_merge_kernel(
+    const float* __restrict__ ws_o, const float* __restrict__ ws_ml,
+    const int32_t* __restrict__ seq_lens, int32_t num_seqs, int32_t hq, int32_t split_keys,
+    int32_t max_splits, uint16_t* __restrict__ out, float* __restrict__ lse) {
+  constexpr int PER = D / 64;  // dims per lane
+  const int64_t item = (int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (item >= (int64_t)num_seqs * hq) return;
+  const int i = (int)(item / hq);
+  const int len = seq_lens[i];
+  const int nsplit = (len + split_keys - 1) / split_keys;
+  if (nsplit <= 1) return;  // written directly by the partial kernel
+  const size_t base = (size_t)item * max_splits;
+  float mmax = -INFINITY;
+  for (int s = 0; s < nsplit; ++s) mmax = fmaxf(mmax, ws_ml[(base + s) * 2]);
+  float den = 0.f;
+  float o[PER];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) o[e] = 0.f;
+  for (int s = 0; s < nsplit; ++s) {
+    const float w = fast_exp2(ws_ml[(base + s) * 2] - mmax);
+    den += w * ws_ml[(base + s) * 2 + 1];
+    const float* src = ws_o + (base + s) * D + lane * PER;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) o[e] += w * src[e];
+  }
+  const float inv = 1.f / den;
+  uint16_t* dst = out + (size_t)item * D + lane * PER;
+  if constexpr (PER == 2) {
+    *reinterpret_cast<uint32_t*>(dst) = pack_bf16x2(o[0] * inv, o[1] * inv);
+  } else {
+    dst[0] = (uint16_t)(pack_bf16x2(o[0] * inv, 0.f) & 0xFFFFu);
+  }
+  if (lse != nullptr && lane == 0) lse[item] = (mmax + log2f(den)) * kLn2;
+}
+
+}  // namespace
+
+int32_t decode_split_keys(int32_t num_seqs, int32_t hkv, int32_t max_seq_len) {
+  // Longest split first; shorten it while the grid would hold too few waves to keep all
+  // 256 compute units streaming (aim for >= 8 waves per unit). A function of the call's
+  // sizes only, so a given call always splits identically.
+  int32_t split = 256;
+  while (split > 64) {
+    const int64_t waves =
+        (int64_t)num_seqs * hkv * ((max_seq_len + split - 1) / split);
+    if (waves >= 2048) break;
+    split /= 2;
+  }
+  return split;
+}
+
+size_t decode_workspace_bytes(int32_t num_seqs, int32_t hq, int32_t hkv, int32_t head_dim,
+                              int32_t max_seq_len) {
+  const int32_t split = decode_split_keys(num_seqs, hkv, max_seq_len);
+  const int64_t max_splits = (max_seq_len + split - 1) / split;
+  if (max_splits <= 1) return 0;
+  return (size_t)num_seqs * hq * max_splits * (head_dim + 2) * sizeof(float);
+}
+
+hipError_t launch_decode(const KvView& kv, const uint16_t* q, int32_t hq,
+                         const int32_t* block_tables, int32_t max_blocks,
+                         const int32_t* seq_lens, int32_t num_seqs, int32_t max_seq_len,
+                         float scale, uint16_t* out, float* lse, void* workspace,
+                         hipStream_t stream) {
+  const int32_t split = decode_split_keys(num_seqs, kv.hkv, max_seq_len);
+  const int32_t max_splits = (max_seq_len + split - 1) / split;
+  float* ws_o = static_cast<float*>(workspace);
+  float* ws_ml = ws_o == nullptr
+                     ? nullptr
+                     : ws_o + (size_t)num_seqs * hq * max_splits * kv.head_dim;
+  const int64_t items = (int64_t)num_seqs * kv.hkv * max_splits;
+  const dim3 grid((unsigned)((items + kWaves - 1) / kWaves));
+  const float scale_log2 = scale * kLog2e;
+  if (kv.head_dim == 128)
+    hipLaunchKernelGGL(decode_partial_kernel<128>, grid, dim3(256), 0, stream, q, kv.k, kv.v,
+                       block_tables, max_blocks, seq_lens, num_seqs, hq, kv.hkv,
+                       kv.num_blocks, split, max_splits, scale_log2, ws_o, ws_ml, out, lse);
+  else
+    hipLaunchKernelGGL(decode_partial_kernel<64>, grid, dim3(256), 0, stream, q, kv.k, kv.v,
+                       block_tables, max_blocks, seq_lens, num_seqs, hq, kv.hkv,
+                       kv.num_blocks, split, max_splits, scale_log2, ws_o, ws_ml, out, lse);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess || max_splits <= 1) return err;
+  const int64_t rows = (int64_t)num_seqs * hq;
+  const dim3 mgrid((unsigned)((rows + kWaves - 1) / kWaves));
+  if (kv.head_dim == 128)
+    hipLaunchKernelGGL(decode_merge_kernel<128>, mgrid, dim3(256), 0, stream, ws_o, ws_ml,
+                       seq_lens, num_seqs, hq, split, max_splits, out, lse);
+  else
+    hipLaunchKernelGGL(decode_merge_kernel<64>, mgrid, dim3(256), 0, stream, ws_o, ws_ml,
+                       seq_lens, num_seqs, hq, split, max_splits, out, lse);
+  return hipGetLastError();
+}
+
+}  // namespace pkv

@@ -1,0 +1,283 @@
+"""Thin ctypes binding of libpkv.so (include/pkv.h), with the C names.
+
+Argument marshalling only: tensors supply device pointers and torch's current stream supplies
+the hipStream_t; every step of the path runs in the library's HIP kernels. There is no CPU
+fallback: importing this module fails if libpkv.so is missing, and the device calls refuse
+tensors that are not on the GPU."""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpkv.so")
+
+if not os.path.exists(_LIB_PATH):
+    raise ImportError(f"{_LIB_PATH} is missing: build it with "
+                      "`python -m paper_2607_23815_amd.build` (needs hipcc)")
+_lib = ctypes.CDLL(_LIB_PATH)
+
+c_int32, c_int64, c_size_t, c_float, c_void_p = (ctypes.c_int32, ctypes.c_int64,
+                                                  ctypes.c_size_t, ctypes.c_float,
+                                                  ctypes.c_void_p)
+P_int32 = ctypes.POINTER(c_int32)
+P_int64 = ctypes.POINTER(c_int64)
+
+PKV_OK = 0
+PKV_ERR_INVALID_ARG = 1
+PKV_ERR_OUT_OF_BLOCKS = 2
+PKV_ERR_SHARED_BLOCK_WRITE = 3
+PKV_ERR_UNSUPPORTED_SHAPE = 4
+PKV_ERR_NOT_FOUND = 5
+PKV_ERR_HIP = 6
+
+
+class PagedKV(ctypes.Structure):
+    _fields_ = [("k_cache", c_void_p), ("v_cache", c_void_p), ("num_blocks", c_int32),
+                ("block_size", c_int32), ("num_kv_heads", c_int32), ("head_dim", c_int32)]
+
+
+_SIGS = {
+    "pkv_last_error": (ctypes.c_char_p, []),
+    "pkv_abi_version": (c_int32, []),
+    "pkv_pool_create": (c_int32, [c_int32, c_int32, P_int32, ctypes.POINTER(c_void_p)]),
+    "pkv_pool_destroy": (None, [c_void_p]),
+    "pkv_pool_num_free": (c_int32, [c_void_p]),
+    "pkv_seq_create": (c_int32, [c_void_p, P_int64]),
+    "pkv_seq_fork": (c_int32, [c_void_p, c_int64, c_int32, P_int64]),
+    "pkv_seq_reserve": (c_int32, [c_void_p, c_int64, c_int32]),
+    "pkv_seq_commit": (c_int32, [c_void_p, c_int64, c_int32]),
+    "pkv_seq_free": (c_int32, [c_void_p, c_int64]),
+    "pkv_seq_len": (c_int32, [c_void_p, c_int64, P_int32]),
+    "pkv_fill_block_tables": (c_int32, [c_void_p, P_int64, c_int32, c_int32, P_int32, P_int32]),
+    "pkv_kv_append": (c_int32, [ctypes.POINTER(PagedKV), c_void_p, c_void_p, c_void_p, c_int32,
+                                c_void_p, c_void_p, c_int32, c_int32, c_int32, c_void_p]),
+    "pkv_prefill_attention": (c_int32, [ctypes.POINTER(PagedKV), c_void_p, c_int32, c_void_p,
+                                        c_int32, c_void_p, c_void_p, c_int32, c_int32, c_int32,
+                                        c_int32, c_float, c_void_p, c_void_p, c_void_p,
+                                        c_size_t, c_void_p]),
+    "pkv_prefill_workspace_bytes": (c_size_t, [c_int32] * 7),
+    "pkv_decode_attention": (c_int32, [ctypes.POINTER(PagedKV), c_void_p, c_int32, c_void_p,
+                                       c_int32, c_void_p, c_int32, c_int32, c_float, c_void_p,
+                                       c_void_p, c_void_p, c_size_t, c_void_p]),
+    "pkv_decode_workspace_bytes": (c_size_t, [c_int32] * 5),
+    "pkv_gather_kv": (c_int32, [ctypes.POINTER(PagedKV), c_void_p, c_int32, c_void_p, c_void_p,
+                                c_int32, c_int32, c_void_p, c_void_p, c_void_p]),
+}
+
+for _name, (_res, _args) in _SIGS.items():
+    _fn = getattr(_lib, _name)
+    _fn.restype = _res
+    _fn.argtypes = _args
+
+EXPORTED = tuple(_SIGS)
+
+
+class PkvError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"[pkv status {status}] {message}")
+        self.status = status
+
+
+def _check(status: int) -> None:
+    if status != PKV_OK:
+        raise PkvError(status, _lib.pkv_last_error().decode())
+
+
+def pkv_last_error() -> str:
+    return _lib.pkv_last_error().decode()
+
+
+def pkv_abi_version() -> int:
+    return int(_lib.pkv_abi_version())
+
+
+# ----------------------------------------------------------------------------------------
+# Block pool
+# ----------------------------------------------------------------------------------------
+class BlockPool:
+    """Host bookkeeping of the KV block pool (pkv_pool_* / pkv_seq_*)."""
+
+    def __init__(self, num_blocks: int, block_size: int = 16,
+                 free_order: Optional[Sequence[int]] = None):
+        handle = c_void_p()
+        arr = None
+        if free_order is not None:
+            arr = np.ascontiguousarray(np.asarray(free_order, dtype=np.int32))
+            ptr = arr.ctypes.data_as(P_int32)
+        else:
+            ptr = None
+        _check(_lib.pkv_pool_create(num_blocks, block_size, ptr, ctypes.byref(handle)))
+        self._h = handle
+        self.num_blocks = num_blocks
+        self.block_size = block_size
+
+    def close(self):
+        if self._h:
+            _lib.pkv_pool_destroy(self._h)
+            self._h = c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def num_free(self) -> int:
+        return int(_lib.pkv_pool_num_free(self._h))
+
+    def create(self) -> int:
+        sid = c_int64()
+        _check(_lib.pkv_seq_create(self._h, ctypes.byref(sid)))
+        return sid.value
+
+    def fork(self, parent: int, shared_tokens: int) -> int:
+        sid = c_int64()
+        _check(_lib.pkv_seq_fork(self._h, parent, shared_tokens, ctypes.byref(sid)))
+        return sid.value
+
+    def reserve(self, seq: int, n: int) -> int:
+        """Returns the status (OK, OUT_OF_BLOCKS or SHARED_BLOCK_WRITE are expected outcomes);
+        raises on argument errors."""
+        st = _lib.pkv_seq_reserve(self._h, seq, n)
+        if st not in (PKV_OK, PKV_ERR_OUT_OF_BLOCKS, PKV_ERR_SHARED_BLOCK_WRITE):
+            _check(st)
+        return st
+
+    def commit(self, seq: int, n: int) -> None:
+        _check(_lib.pkv_seq_commit(self._h, seq, n))
+
+    def free(self, seq: int) -> None:
+        _check(_lib.pkv_seq_free(self._h, seq))
+
+    def seq_len(self, seq: int) -> int:
+        n = c_int32()
+        _check(_lib.pkv_seq_len(self._h, seq, ctypes.byref(n)))
+        return n.value
+
+    def block_tables(self, seq_ids: Sequence[int], max_blocks: int):
+        """(tables int32 [n][max_blocks] padded -1, committed lengths int32 [n])."""
+        ids = np.ascontiguousarray(np.asarray(seq_ids, dtype=np.int64))
+        n = ids.shape[0]
+        tables = np.empty((n, max_blocks), dtype=np.int32)
+        lens = np.empty(n, dtype=np.int32)
+        _check(_lib.pkv_fill_block_tables(self._h, ids.ctypes.data_as(P_int64), n, max_blocks,
+                                          tables.ctypes.data_as(P_int32),
+                                          lens.ctypes.data_as(P_int32)))
+        return tables, lens
+
+
+# ----------------------------------------------------------------------------------------
+# Device calls (torch tensors on the GPU)
+# ----------------------------------------------------------------------------------------
+def _dev_ptr(t, name, dtype=None):
+    import torch
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise TypeError(f"{name} must be a GPU tensor (the library has no CPU path)")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return c_void_p(s.cuda_stream)
+
+
+def paged_kv(k_cache, v_cache) -> PagedKV:
+    """Describe a pool: k_cache bf16 [num_blocks][Hkv][D/8][16][8], v_cache bf16
+    [num_blocks][Hkv][D][16]."""
+    import torch
+    if k_cache.dim() != 5 or v_cache.dim() != 4:
+        raise ValueError("k_cache must be [nb][Hkv][D/8][bs][8] and v_cache [nb][Hkv][D][bs]")
+    nb, hkv, nch, bs, e = k_cache.shape
+    if e != 8 or tuple(v_cache.shape) != (nb, hkv, nch * 8, bs):
+        raise ValueError("k_cache / v_cache shapes disagree")
+    kp = _dev_ptr(k_cache, "k_cache", torch.bfloat16)
+    vp = _dev_ptr(v_cache, "v_cache", torch.bfloat16)
+    return PagedKV(kp, vp, nb, bs, hkv, nch * 8)
+
+
+def pkv_kv_append(k_cache, v_cache, k_new, v_new, block_tables, cached_lens, cu_new_lens,
+                  max_new_len: int, stream=None) -> None:
+    import torch
+    kv = paged_kv(k_cache, v_cache)
+    b = int(cached_lens.shape[0])
+    _check(_lib.pkv_kv_append(ctypes.byref(kv), _dev_ptr(k_new, "k_new", torch.bfloat16),
+                              _dev_ptr(v_new, "v_new", torch.bfloat16),
+                              _dev_ptr(block_tables, "block_tables", torch.int32),
+                              int(block_tables.shape[1]),
+                              _dev_ptr(cached_lens, "cached_lens", torch.int32),
+                              _dev_ptr(cu_new_lens, "cu_new_lens", torch.int32), b,
+                              int(k_new.shape[0]), int(max_new_len), _stream(stream)))
+
+
+def pkv_prefill_workspace_bytes(num_seqs, total_new, num_q_heads, num_kv_heads, head_dim,
+                                max_new_len, max_total_len) -> int:
+    return int(_lib.pkv_prefill_workspace_bytes(num_seqs, total_new, num_q_heads, num_kv_heads,
+                                                head_dim, max_new_len, max_total_len))
+
+
+def pkv_prefill_attention(k_cache, v_cache, q, block_tables, cached_lens, cu_new_lens,
+                          max_new_len: int, max_total_len: int, scale: float, out, lse=None,
+                          workspace=None, stream=None) -> None:
+    import torch
+    kv = paged_kv(k_cache, v_cache)
+    t, hq, d = q.shape
+    b = int(cached_lens.shape[0])
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(_lib.pkv_prefill_attention(
+        ctypes.byref(kv), _dev_ptr(q, "q", torch.bfloat16), hq,
+        _dev_ptr(block_tables, "block_tables", torch.int32), int(block_tables.shape[1]),
+        _dev_ptr(cached_lens, "cached_lens", torch.int32),
+        _dev_ptr(cu_new_lens, "cu_new_lens", torch.int32), b, t, int(max_new_len),
+        int(max_total_len), float(scale), _dev_ptr(out, "out", torch.bfloat16),
+        _dev_ptr(lse, "lse", torch.float32), _dev_ptr(workspace, "workspace"), ws_bytes,
+        _stream(stream)))
+
+
+def pkv_decode_workspace_bytes(num_seqs, num_q_heads, num_kv_heads, head_dim,
+                               max_seq_len) -> int:
+    return int(_lib.pkv_decode_workspace_bytes(num_seqs, num_q_heads, num_kv_heads, head_dim,
+                                               max_seq_len))
+
+
+def pkv_decode_attention(k_cache, v_cache, q, block_tables, seq_lens, max_seq_len: int,
+                         scale: float, out, lse=None, workspace=None, stream=None) -> None:
+    import torch
+    kv = paged_kv(k_cache, v_cache)
+    b, hq, d = q.shape
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(_lib.pkv_decode_attention(
+        ctypes.byref(kv), _dev_ptr(q, "q", torch.bfloat16), hq,
+        _dev_ptr(block_tables, "block_tables", torch.int32), int(block_tables.shape[1]),
+        _dev_ptr(seq_lens, "seq_lens", torch.int32), b, int(max_seq_len), float(scale),
+        _dev_ptr(out, "out", torch.bfloat16), _dev_ptr(lse, "lse", torch.float32),
+        _dev_ptr(workspace, "workspace"), ws_bytes, _stream(stream)))
+
+
+def pkv_gather_kv(k_cache, v_cache, block_tables, lens, cu_lens, max_len: int, k_out, v_out,
+                  stream=None) -> None:
+    import torch
+    kv = paged_kv(k_cache, v_cache)
+    _check(_lib.pkv_gather_kv(ctypes.byref(kv), _dev_ptr(block_tables, "block_tables",
+                                                         torch.int32),
+                              int(block_tables.shape[1]), _dev_ptr(lens, "lens", torch.int32),
+                              _dev_ptr(cu_lens, "cu_lens", torch.int32), int(lens.shape[0]),
+                              int(max_len), _dev_ptr(k_out, "k_out", torch.bfloat16),
+                              _dev_ptr(v_out, "v_out", torch.bfloat16), _stream(stream)))
+
+
+def alloc_workspace(nbytes: int, device="cuda"):
+    """A byte tensor for the workspace argument (None when nbytes is 0)."""
+    import torch
+    if nbytes == 0:
+        return None
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)

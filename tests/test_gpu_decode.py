@@ -1,0 +1,100 @@
+"""GPU tier: paged split-K decode attention through the C ABI against the fp64 oracle.
+
+Each case appends the step's token (position C_i) and then attends over all C_i + 1 keys.
+Lengths straddle every split and block boundary; the bar is the prefill bar."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from tests.gpu_util import (DevBatch, bf16_to_f64, compare, dev_pools, i32, say, scale_for,
+                            to_host_bits)
+
+pytestmark = pytest.mark.gpu
+
+
+def run_decode(lib, case, bi=0, pools=None):
+    import torch
+    b = case.batches[bi]
+    pk, pv = pools if pools is not None else dev_pools(case)
+    db = DevBatch(b)
+    nseq = b.n_seqs
+    seq_lens = b.prefix_lens + 1
+    max_len = int(seq_lens.max())
+    out = torch.empty((nseq, case.hq, case.d), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((nseq, case.hq), dtype=torch.float32, device="cuda")
+    ws = lib.alloc_workspace(lib.pkv_decode_workspace_bytes(nseq, case.hq, case.hkv, case.d,
+                                                            max_len))
+    lib.pkv_kv_append(pk, pv, db.k_new, db.v_new, db.tables, db.cached, db.cu, 1)
+    lib.pkv_decode_attention(pk, pv, db.q, db.tables, i32(seq_lens), max_len,
+                             scale_for(case.d), out, lse=lse, workspace=ws)
+    torch.cuda.synchronize()
+    return to_host_bits(out), lse.cpu().numpy().astype(np.float64)
+
+
+def oracle_decode(case, bi=0):
+    b = case.batches[bi]
+    return oracle.decode_attention(case.pool_k, case.pool_v, b.block_tables, b.prefix_lens,
+                                   b.q, b.k_new, b.v_new, scale_for(case.d), case.bs)
+
+
+def check(name, got, ref):
+    compare(name + " out", bf16_to_f64(got[0]), ref[0])
+    compare(name + " lse", got[1], ref[1], atol_max=2e-3, atol_mean=2e-4)
+
+
+@pytest.mark.parametrize("spec", [W.LLAMA3_8B_DECODE.scaled(decode=48),
+                                  W.MIXED_70B.scaled(prefill=0, decode=24)],
+                         ids=lambda s: s.name)
+def test_decode_matches_oracle(gpu_lib, spec):
+    say(f"[decode] {spec.name}")
+    case = W.make_case(spec)
+    bi = [k for k, b in enumerate(case.batches) if b.kind == "decode"][0]
+    check(spec.name, run_decode(gpu_lib, case, bi), oracle_decode(case, bi))
+
+
+CONTEXTS = [0, 1, 14, 15, 16, 17, 30, 31, 32, 33, 63, 64, 127, 255, 256, 257, 511, 512, 1000,
+            2047, 2048, 4095]
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (64, 8, 128), (4, 2, 64), (16, 1, 128)])
+def test_decode_split_and_block_boundaries(gpu_lib, hq, hkv, d):
+    say(f"[decode] boundaries hq={hq} hkv={hkv} d={d}")
+    spec = W.WorkloadSpec(f"decode_edges_{hq}_{hkv}_{d}", 140 + hq + d, hq, hkv, d,
+                          (W.BatchSpec("decode", len(CONTEXTS), W.Dist.const(1),
+                                       W.Dist.const(1)),), ("scale", 1.25))
+    case = W.make_case(spec, prefix_override=[CONTEXTS])
+    check(spec.name, run_decode(gpu_lib, case), oracle_decode(case))
+
+
+def test_decode_small_batch_uses_short_splits(gpu_lib):
+    """Few sequences -> the split shrinks to keep the grid full; results must not change
+    beyond rounding."""
+    say("[decode] small batch")
+    spec = W.WorkloadSpec("decode_small", 150, 32, 8, 128,
+                          (W.BatchSpec("decode", 2, W.Dist.const(1), W.Dist.const(1)),),
+                          ("scale", 1.25))
+    case = W.make_case(spec, prefix_override=[[3000, 77]])
+    check(spec.name, run_decode(gpu_lib, case), oracle_decode(case))
+
+
+def test_decode_is_deterministic(gpu_lib):
+    say("[decode] determinism")
+    spec = W.LLAMA3_8B_DECODE.scaled(decode=16)
+    a = run_decode(gpu_lib, W.make_case(spec))
+    b = run_decode(gpu_lib, W.make_case(spec))
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+def test_decode_equals_single_token_prefill(gpu_lib):
+    """One decode step == a prefill of one new token over the same cache (both within the
+    tolerance of the oracle, and of each other)."""
+    from tests.test_gpu_prefill import run_prefill
+    say("[decode] == prefill N=1")
+    spec = W.LLAMA3_8B_DECODE.scaled(decode=12)
+    case = W.make_case(spec)
+    d_out, _ = run_decode(gpu_lib, case)
+    case2 = W.make_case(spec)
+    case2.batches[0].kind = "prefill"
+    p_out, _ = run_prefill(gpu_lib, case2)
+    compare("decode vs prefill", bf16_to_f64(d_out), bf16_to_f64(p_out))
