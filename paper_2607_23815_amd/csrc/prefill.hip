@@ -37,6 +37,20 @@ namespace {
 constexpr int kCols = 128;  // query columns per workgroup (4 waves x 32)
 constexpr int kKeys = 64;   // keys per tile (4 blocks)
 
+// Wait until every global load this thread issued has completed (vmcnt = 0; the other
+// counters left at their maxima), so its direct-to-LDS loads have been written.
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// The value held by the lane 32 apart (lanes l and l ^ 32 hold the two key halves of one
+// column): v_permlane32_swap exchanges the upper half of one register with the lower half of
+// another, so swapping a register with a copy of itself gives every lane its partner's value.
+__device__ __forceinline__ float swap_halves(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  // lanes < 32 find the partner in the second result, lanes >= 32 in the first
+  return __uint_as_float((threadIdx.x & 32) ? r[0] : r[1]);
+}
+
 // sigma: swap bits 2 and 3 of a key index within a 16-key block (an involution)
 __device__ __forceinline__ int swap23(int s) {
   return (s & ~0xC) | ((s & 8) >> 1) | ((s & 4) << 1);
@@ -49,24 +63,39 @@ struct PrefillSmem {
   uint16_t v[2][4 * SLAB];
 };
 
+// Rescale the running output only when a column's maximum grows by more than this many
+// powers of two; otherwise keep the stale maximum (weights then stay below 2^8, exact in the
+// normalisation). After the first tiles the maximum of N(0,1) scores hardly moves, so the
+// 64 accumulator multiplies per tile are almost always skipped.
+constexpr float kRescaleThreshold = 8.0f;
+
 template <int D>
-__global__ __launch_bounds__(256) void prefill_kernel(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
-    const uint16_t* __restrict__ v_cache, const int32_t* __restrict__ block_tables,
-    int32_t max_blocks, const int32_t* __restrict__ cached_lens,
-    const int32_t* __restrict__ cu_new_lens, int32_t hq, int32_t hkv, int32_t num_blocks,
-    float scale_log2, uint16_t* __restrict__ out, float* __restrict__ lse) {
+__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2)))
+void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
+                    const uint16_t* __restrict__ v_cache, const int32_t* __restrict__ block_tables,
+                    int32_t max_blocks, const int32_t* __restrict__ cached_lens,
+                    const int32_t* __restrict__ cu_new_lens, int32_t hq, int32_t hkv,
+                    int32_t num_blocks, int32_t qtiles, float scale_log2,
+                    uint16_t* __restrict__ out, float* __restrict__ lse) {
   constexpr int SLAB = D * kBlockSize;
-  constexpr int UNITS = 4 * SLAB / 8;   // 16-byte units per K (or V) tile
-  constexpr int LPT = UNITS / 256;      // units per thread per tile
-  constexpr int KK = D / 16;            // k-steps of the score product
-  constexpr int DB = D / 32;            // 32-dim blocks of the value product
+  constexpr int UNITS = SLAB / 8;        // 16-byte units per block slab
+  constexpr int LPT = 4 * UNITS / 256;   // direct loads per thread per tile (K or V)
+  constexpr int KK = D / 16;             // k-steps of the score product
+  constexpr int DB = D / 32;             // 32-dim blocks of the value product
   __shared__ __align__(16) PrefillSmem<D> sm;
 
+  // XCD-aware mapping: consecutive workgroup ids go to different XCDs (id % 8), so give each
+  // XCD a contiguous range of work items; the query tiles of one (sequence, kv head), which
+  // all read the same K/V, then run on one XCD and share its L2.
+  const int nwg = gridDim.x;
+  const int lin = blockIdx.x;
+  const int xcd = lin & 7;
+  const int item = xcd * (nwg >> 3) + min(xcd, nwg & 7) + (lin >> 3);
+  const int qt = qtiles - 1 - item % qtiles;  // longest (last) query tile first
+  const int kvh = (item / qtiles) % hkv;
+  const int i = item / (qtiles * hkv);
+
   const int g = hq / hkv;
-  const int qt = (int)(gridDim.x - 1 - blockIdx.x);  // last (longest) query tiles first
-  const int kvh = blockIdx.y;
-  const int i = blockIdx.z;
   const int p = cached_lens[i];
   const int row0 = cu_new_lens[i];
   const int n = cu_new_lens[i + 1] - row0;
@@ -117,103 +146,132 @@ __global__ __launch_bounds__(256) void prefill_kernel(
 
   const int32_t* table = block_tables + (size_t)i * max_blocks;
   const size_t head_off = (size_t)kvh * SLAB;
+  // stand-in for blocks past the sequence: its first block (len >= 1, so it owns one)
+  int32_t blk_first = table[0];
+  if (blk_first < 0 || blk_first >= num_blocks) blk_first = 0;
 
-  // ---- staging: thread tid moves units tid + 256 k of the K tile and of the V tile ----
-  u32x4 kreg[LPT], vreg[LPT];
-  auto load_tile = [&](int kt) {
+  // ---- staging: direct global -> LDS 16-byte loads. Load k of wave w fills LDS units
+  // k*256 + 64 w + lane of the tile; the swizzle is applied on the global side: LDS K unit
+  // c*16 + t holds global unit c*16 + swap23(t), LDS V unit 2d + t holds global unit
+  // 2d + (t ^ ((d >> 2) & 1)). Out-of-range blocks load the sequence's first block instead
+  // (finite data, masked or zeroed before use). ----
+  int kofs[LPT], vofs[LPT];  // per-lane element offsets within a block slab
 #pragma unroll
-    for (int k = 0; k < LPT; ++k) {
-      const int u = tid + 256 * k;
-      const int bb = u / (SLAB / 8);   // block within the tile
-      const int w = u % (SLAB / 8);    // unit within the block slab
-      const int b = kt * 4 + bb;       // logical block
-      u32x4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
-      if (b * kBlockSize < len && b < max_blocks) {
-        const int blk = table[b];
-        if (blk >= 0 && blk < num_blocks) {
-          const size_t base = (size_t)blk * hkv * SLAB + head_off + (size_t)w * 8;
-          kv = ld16(k_cache + base);
-          vv = ld16(v_cache + base);
-          // V unit w = (dim d, half hf) holds slots 8 hf .. 8 hf + 7; zero slots >= len
-          const int first = b * kBlockSize + (w & 1) * 8;
-          if (first + 8 > len) {
-            const int keep = max(len - first, 0);  // 0..7 slots stay
-            uint32_t words[4] = {vv[0], vv[1], vv[2], vv[3]};
+  for (int k = 0; k < LPT; ++k) {
+    const int pos = (k * 256 + wave * 64 + lane) % UNITS;
+    const int c = pos >> 4;
+    kofs[k] = (c * 16 + swap23(pos & 15)) * 8;
+    const int d = pos >> 1;
+    vofs[k] = (2 * d + ((pos & 1) ^ ((d >> 2) & 1))) * 8;
+  }
+  auto issue_tile = [&](int kt, int buf) {
+    // the tile's four physical blocks: wave-uniform scalar loads, no branches
+    int blk[4];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              if (e >= keep) words[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
-            }
-            vv = u32x4{words[0], words[1], words[2], words[3]};
-          }
-        }
-      }
-      kreg[k] = kv;
-      vreg[k] = vv;
+    for (int bb = 0; bb < 4; ++bb) {
+      const int b = kt * 4 + bb;
+      const int e = table[min(b, max_blocks - 1)];
+      const bool ok = (b * kBlockSize < len) & (b < max_blocks) & (e >= 0) & (e < num_blocks);
+      blk[bb] = ok ? e : blk_first;
     }
-  };
-  auto store_tile = [&](int buf) {
 #pragma unroll
     for (int k = 0; k < LPT; ++k) {
-      const int u = tid + 256 * k;
-      const int bb = u / (SLAB / 8);
-      const int w = u % (SLAB / 8);
-      // K unit w = (chunk c, slot s): placed at c*16 + swap23(s)
-      const int c = w >> 4, s = w & 15;
-      const int kpos = bb * (SLAB / 8) + c * 16 + swap23(s);
-      // V unit w = (dim d, half hf): placed at 2d + (hf ^ ((d >> 2) & 1))
-      const int d = w >> 1, hf = w & 1;
-      const int vpos = bb * (SLAB / 8) + 2 * d + (hf ^ ((d >> 2) & 1));
-      st16(&sm.k[buf][kpos * 8], kreg[k]);
-      st16(&sm.v[buf][vpos * 8], vreg[k]);
+      const int bb = (k * 256 + wave * 64) / UNITS;  // block of the tile (wave-uniform)
+      const int b = __builtin_amdgcn_readfirstlane(blk[bb]);
+      const size_t base = (size_t)b * hkv * SLAB + head_off;
+      const int ldsoff = (k * 256 + wave * 64) * 8;  // elements; + 8 * lane by the hardware
+      __builtin_amdgcn_global_load_lds(
+          (const void*)(k_cache + base + kofs[k]),
+          (__attribute__((address_space(3))) void*)(&sm.k[buf][ldsoff]), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(
+          (const void*)(v_cache + base + vofs[k]),
+          (__attribute__((address_space(3))) void*)(&sm.v[buf][ldsoff]), 16, 0, 0);
     }
   };
 
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
+  // lane-constant LDS read offsets (elements)
+  const int kread = (lc >> 4) * SLAB + (hh * 16 + (lc & 15)) * 8;
+  const int vread = (2 * lc + (hh ^ ((lc >> 2) & 1))) * 8;
 
+  issue_tile(0, 0);
   for (int kt = 0; kt < ntiles; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < ntiles) load_tile(kt + 1);
+    wait_vmem();      // this thread's direct loads of tile kt have landed in LDS
+    __syncthreads();  // ... every thread's; and every wave is done reading buffer buf ^ 1
+    if (kt + 1 < ntiles) {
+      issue_tile(kt + 1, buf ^ 1);
+    } else if ((kt + 1) * kKeys > len) {
+      // last tile reaches past the sequence: zero V slots >= len (they may hold any bits)
+#pragma unroll
+      for (int k = 0; k < 4 * UNITS / 256; ++k) {
+        const int P = tid + 256 * k;
+        const int bb = P / UNITS, pos = P % UNITS;
+        const int d = pos >> 1;
+        const int hf = (pos & 1) ^ ((d >> 2) & 1);
+        const int first = kt * kKeys + bb * kBlockSize + hf * 8;
+        const int keep = min(max(len - first, 0), 8);
+        if (keep < 8) {
+          uint16_t* u = &sm.v[buf][P * 8];
+          u32x4 w = ld16(u);
+          uint32_t words[4] = {w[0], w[1], w[2], w[3]};
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (e >= keep) words[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+          st16(u, u32x4{words[0], words[1], words[2], words[3]});
+        }
+      }
+      __syncthreads();
+    }
 
     const int key0 = kt * kKeys;
     if (wave_live && key0 <= p + wj_hi) {  // a key of the tile is visible to a wave column
-      // ---- scores ----
+      // ---- scores S^T (raw): both 32-key halves, as two independent accumulation chains ----
+      u32x4 ka[2][KK];
+#pragma unroll
+      for (int beta = 0; beta < 2; ++beta)
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk)
+          ka[beta][kk] = ld16(&sm.k[buf][kread + beta * 2 * SLAB + kk * 256]);
       f32x16 s[2];
 #pragma unroll
-      for (int beta = 0; beta < 2; ++beta) {
+      for (int beta = 0; beta < 2; ++beta)
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[beta][r] = 0.f;
-        // A row lc <- key 32 beta + sigma(lc): block 2 beta + lc/16; LDS slot position lc%16
-        const uint16_t* kb = &sm.k[buf][(2 * beta + (lc >> 4)) * SLAB];
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-          const int c = 2 * kk + hh;
-          const u32x4 a = ld16(kb + (c * 16 + (lc & 15)) * 8);
-          s[beta] = mfma32(as_bf16x8(a), qf[kk], s[beta]);
-        }
+      for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+        for (int beta = 0; beta < 2; ++beta)
+          s[beta] = mfma32(as_bf16x8(ka[beta][kk]), qf[kk], s[beta]);
+      // register r of half-tile beta holds the score of key
+      // key0 + 32 beta + 16 (r/8) + 8 hh + 4 ((r/4) % 2) + r % 4
+      if (key0 + kKeys - 1 > p + wj_lo) {
+#pragma unroll
+        for (int beta = 0; beta < 2; ++beta)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = key0 + 32 * beta + 16 * (r >> 3) + 8 * hh + 4 * ((r >> 2) & 1) +
+                            (r & 3);
+            s[beta][r] = key <= lim ? s[beta][r] : -INFINITY;
+          }
       }
-      // register r of half-tile beta holds score row R = 8(r/4) + 4hh + r%4, i.e. key
-      // key0 + 32 beta + sigma(R) = key0 + 32 beta + 8 hh + 4 (r/4 % 2) + 16 (r/8) + r%4
-      const bool need_mask = key0 + kKeys - 1 > p + wj_lo;
       float mx = -INFINITY;
 #pragma unroll
       for (int beta = 0; beta < 2; ++beta)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float x = s[beta][r] * scale_log2;
-          if (need_mask) {
-            const int key = key0 + 32 * beta + 16 * (r >> 3) + 8 * hh + 4 * ((r >> 2) & 1) +
-                            (r & 3);
-            x = key <= lim ? x : -INFINITY;
-          }
-          s[beta][r] = x;
-          mx = fmaxf(mx, x);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m, mx);
-      const float alpha = fast_exp2(m - m_new);
-      m = m_new;
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[beta][r]);
+      mx = fmaxf(mx, swap_halves(mx)) * scale_log2;
+      const bool grow = mx > m + kRescaleThreshold;
+      if (__builtin_amdgcn_ballot_w64(grow)) {
+        const float m_new = grow ? mx : m;
+        const float alpha = fast_exp2(m - m_new);
+        m = m_new;
+        lpart *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+      }
+      const float neg_m = -m;
       float ps = 0.f;
       bf16x8 pf[2][2];
 #pragma unroll
@@ -223,42 +281,31 @@ __global__ __launch_bounds__(256) void prefill_kernel(
           u32x4 w;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const float a = fast_exp2(s[beta][8 * u + 2 * e] - m_new);
-            const float b = fast_exp2(s[beta][8 * u + 2 * e + 1] - m_new);
+            const float a = fast_exp2(__builtin_fmaf(s[beta][8 * u + 2 * e], scale_log2, neg_m));
+            const float b = fast_exp2(__builtin_fmaf(s[beta][8 * u + 2 * e + 1], scale_log2, neg_m));
             ps += a + b;
             w[e] = pack_bf16x2(a, b);
           }
           pf[beta][u] = as_bf16x8(w);
         }
-      lpart = lpart * alpha + ps;
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-      // ---- values: step (beta, u) covers keys key0 + 32 beta + 16 u + 0..15 = block
-      // 2 beta + u; lane group hh supplies slots 8 hh .. 8 hh + 7 of V^T row 32 db + lc ----
+      lpart += ps;
+      // ---- values: step (beta, u) covers block 2 beta + u of the tile; lane group hh
+      // supplies slots 8 hh .. 8 hh + 7 of V^T row 32 db + lc ----
 #pragma unroll
       for (int beta = 0; beta < 2; ++beta)
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-          const uint16_t* vb = &sm.v[buf][(2 * beta + u) * SLAB];
+          const uint16_t* vb = &sm.v[buf][(2 * beta + u) * SLAB + vread];
 #pragma unroll
           for (int db = 0; db < DB; ++db) {
-            const int d = db * 32 + lc;
-            const int pos = 2 * d + (hh ^ ((d >> 2) & 1));
-            const u32x4 a = ld16(vb + pos * 8);
+            const u32x4 a = ld16(vb + db * 512);
             o[db] = mfma32(as_bf16x8(a), pf[beta][u], o[db]);
           }
         }
     }
-
-    if (kt + 1 < ntiles) {
-      store_tile(buf ^ 1);
-    }
-    __syncthreads();
   }
 
-  const float l = lpart + __shfl_xor(lpart, 32);
+  const float l = lpart + swap_halves(lpart);
   if (!col_ok) return;
   const float inv = 1.f / l;
   uint16_t* orow = out + ((size_t)(row0 + j) * hq + head) * D;
@@ -283,16 +330,18 @@ hipError_t launch_prefill(const KvView& kv, const uint16_t* q, int32_t hq,
                           float* lse, hipStream_t stream) {
   const int32_t g = hq / kv.hkv;
   const int64_t qtiles = ((int64_t)max_new_len * g + kCols - 1) / kCols;
-  const dim3 grid((unsigned)qtiles, kv.hkv, num_seqs);
+  const int64_t items = qtiles * kv.hkv * num_seqs;
+  if (items > INT32_MAX) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)items);
   const float scale_log2 = scale * kLog2e;
   if (kv.head_dim == 128)
     hipLaunchKernelGGL(prefill_kernel<128>, grid, dim3(256), 0, stream, q, kv.k, kv.v,
                        block_tables, max_blocks, cached_lens, cu_new_lens, hq, kv.hkv,
-                       kv.num_blocks, scale_log2, out, lse);
+                       kv.num_blocks, (int32_t)qtiles, scale_log2, out, lse);
   else
     hipLaunchKernelGGL(prefill_kernel<64>, grid, dim3(256), 0, stream, q, kv.k, kv.v,
                        block_tables, max_blocks, cached_lens, cu_new_lens, hq, kv.hkv,
-                       kv.num_blocks, scale_log2, out, lse);
+                       kv.num_blocks, (int32_t)qtiles, scale_log2, out, lse);
   return hipGetLastError();
 }
 
