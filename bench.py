@@ -15,6 +15,8 @@ the CPU oracle timed on a bounded sample of the same workload, and secondary wor
 (paged decode, the mixed 70B-shaped batch, long documents with a shared prompt).
 
     python bench.py [--steps K] [--warmup W] [--no-secondary] [--no-cpu-baseline]
+    python bench.py --profile-kernel {prefill,decode,append} [--workload NAME] [--steps K]
+        (launches only that kernel, for rocprofv3 kernel-trace and counter passes)
 """
 import argparse
 import hashlib
@@ -420,6 +422,62 @@ def secondary(args, lib, torch):
     return out
 
 
+def profile_copy(args, torch):
+    """A plain device copy of known size (1 GiB read + 1 GiB written per launch): the
+    reference that scales the L2<->HBM byte counters to bytes."""
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    stream = torch.cuda.current_stream()
+    _, _, per = time_events(torch, stream, [lambda: b.copy_(a)], args.steps, args.warmup)
+    print(json.dumps({"kernel": "copy", "bytes_read": n, "bytes_written": n,
+                      "launches": args.steps + args.warmup, "avg_ms": per[0] * 1e3,
+                      "GB_s": 2 * n / per[0] / 1e9}), flush=True)
+
+
+def profile_kernel(args, lib, torch):
+    """Launch one kernel of the hot path `steps` times on one workload (for rocprofv3)."""
+    import workloads as W
+    if args.profile_kernel == "copy":
+        return profile_copy(args, torch)
+    spec = W.BY_NAME[args.workload]
+    wl = Workload(spec, lib, torch)
+    kind = "decode" if args.profile_kernel == "decode" else "prefill"
+    bi = [k for k, (b, _) in enumerate(wl.batches) if b.kind == kind]
+    if not bi:
+        raise SystemExit(f"{spec.name} has no {kind} batch")
+    b, _ = wl.batches[bi[0]]
+    dv = wl.dev[bi[0]]
+    pk, pv = wl.case.pool_k, wl.case.pool_v
+    from tests.gpu_util import i32
+    if args.profile_kernel == "append":
+        fn = lambda: lib.pkv_kv_append(pk, pv, b.k_new, b.v_new, dv["tables"], dv["cached"],
+                                       dv["cu"], max(dv["max_new"], 1))
+    elif args.profile_kernel == "prefill":
+        out = torch.empty((b.total_new, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
+        lib.pkv_kv_append(pk, pv, b.k_new, b.v_new, dv["tables"], dv["cached"], dv["cu"],
+                          dv["max_new"])
+        fn = lambda: lib.pkv_prefill_attention(pk, pv, b.q, dv["tables"], dv["cached"],
+                                               dv["cu"], dv["max_new"], dv["max_total"],
+                                               wl.scale, out)
+    else:
+        seq_lens = b.prefix_lens + 1
+        maxl = int(seq_lens.max())
+        sl = i32(seq_lens)
+        out = torch.empty((b.n_seqs, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
+        ws = lib.alloc_workspace(lib.pkv_decode_workspace_bytes(b.n_seqs, wl.hq, wl.hkv, wl.d,
+                                                                maxl))
+        lib.pkv_kv_append(pk, pv, b.k_new, b.v_new, dv["tables"], dv["cached"], dv["cu"], 1)
+        fn = lambda: lib.pkv_decode_attention(pk, pv, b.q, dv["tables"], sl, maxl, wl.scale,
+                                              out, workspace=ws)
+    stream = torch.cuda.current_stream()
+    _, gpu, per = time_events(torch, stream, [fn], args.steps, args.warmup)
+    print(json.dumps({"workload": spec.name, "kernel": args.profile_kernel,
+                      "launches": args.steps + args.warmup, "avg_ms": per[0] * 1e3}),
+          flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -427,6 +485,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-kernel", choices=("prefill", "decode", "append", "copy"))
+    ap.add_argument("--workload", default="llama3_8b_prefix_reuse_prefill")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this path needs no collective and runs one "
@@ -437,6 +497,9 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     from paper_2607_23815_amd import lib
+    if args.profile_kernel:
+        profile_kernel(args, lib, torch)
+        return
     log(f"[bench] primary workload, steps={args.steps} warmup={args.warmup}")
     res, wl, dec = primary(args, lib, torch)
     log(f"[bench] primary done: {res['ms_per_step']:.3f} ms/step")

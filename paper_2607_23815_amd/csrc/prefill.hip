@@ -28,6 +28,8 @@
 // bits (NaN included) never meet a zero weight inside the matrix core.
 #include <math.h>
 
+#include <type_traits>
+
 #include "device_utils.h"
 #include "launch.h"
 
@@ -69,6 +71,13 @@ struct PrefillSmem {
 // 64 accumulator multiplies per tile are almost always skipped.
 constexpr float kRescaleThreshold = 8.0f;
 
+// Sum of the two bf16 values packed in w, added to acc (v_dot2 with (1, 1)).
+__device__ __forceinline__ float add_pair_bf16(uint32_t w, float acc) {
+  typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), one, acc, false);
+}
+
 template <int D>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2)))
 void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
@@ -105,7 +114,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
   const int len = p + n;
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int lane = tid & 63;
   const int lc = lane & 31;
   const int hh = lane >> 5;
@@ -120,8 +129,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
   const int nkeys = p + jmax + 1;
   const int ntiles = (nkeys + kKeys - 1) / kKeys;
   const int wcol0 = col0 + wave * 32;
-  const int wj_lo = min(wcol0 / g, n - 1);        // earliest token among the wave's columns
-  const int wj_hi = min((wcol0 + 31) / g, n - 1); // latest
+  const int wj_lo = min(wcol0 / g, n - 1);         // earliest token among the wave's columns
   const bool wave_live = wcol0 < ncols;            // the wave has at least one real column
 
   // Q as the B operand of S^T = K Q^T: lane holds Q[column lc][16 kk + 8 hh .. +7]
@@ -150,158 +158,261 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
   int32_t blk_first = table[0];
   if (blk_first < 0 || blk_first >= num_blocks) blk_first = 0;
 
-  // ---- staging: direct global -> LDS 16-byte loads. Load k of wave w fills LDS units
-  // k*256 + 64 w + lane of the tile; the swizzle is applied on the global side: LDS K unit
+  // ---- staging: direct global -> LDS 16-byte loads. Wave w stages block w of every tile:
+  // its load k fills LDS units 64 k + lane of that block's slab (the whole 4 KB slab at
+  // head_dim 128 in four loads). The bank swizzle is applied on the global side: LDS K unit
   // c*16 + t holds global unit c*16 + swap23(t), LDS V unit 2d + t holds global unit
-  // 2d + (t ^ ((d >> 2) & 1)). Out-of-range blocks load the sequence's first block instead
-  // (finite data, masked or zeroed before use). ----
-  int kofs[LPT], vofs[LPT];  // per-lane element offsets within a block slab
+  // 2d + (t ^ ((d >> 3) & 1)); with these, the 16 lanes the LDS serves per cycle read 16
+  // distinct 16-byte bank groups. ----
+  constexpr int WLOADS = UNITS / 64;     // loads per wave per block slab
+  int kofs[WLOADS], vofs[WLOADS];        // per-lane element offsets within a block slab
 #pragma unroll
-  for (int k = 0; k < LPT; ++k) {
-    const int pos = (k * 256 + wave * 64 + lane) % UNITS;
+  for (int k = 0; k < WLOADS; ++k) {
+    const int pos = k * 64 + lane;
     const int c = pos >> 4;
     kofs[k] = (c * 16 + swap23(pos & 15)) * 8;
     const int d = pos >> 1;
-    vofs[k] = (2 * d + ((pos & 1) ^ ((d >> 2) & 1))) * 8;
+    vofs[k] = (2 * d + ((pos & 1) ^ ((d >> 3) & 1))) * 8;
   }
-  auto issue_tile = [&](int kt, int buf) {
-    // the tile's four physical blocks: wave-uniform scalar loads, no branches
-    int blk[4];
-#pragma unroll
-    for (int bb = 0; bb < 4; ++bb) {
-      const int b = kt * 4 + bb;
-      const int e = table[min(b, max_blocks - 1)];
-      const bool ok = (b * kBlockSize < len) & (b < max_blocks) & (e >= 0) & (e < num_blocks);
-      blk[bb] = ok ? e : blk_first;
+  // Block-table entries through a per-wave register table: lane l of a chunk holds entry
+  // 64 c + l, already checked (entries past the sequence, past the table or out of the pool
+  // are replaced by the sequence's first block: finite data, masked or zeroed before use).
+  // A chunk covers 16 tiles; the K and V streams keep one chunk each.
+  auto load_chunk = [&](int c) {
+    const int e = c * 64 + lane;
+    int v = blk_first;
+    if (e < max_blocks && e * kBlockSize < len) {
+      const int t = table[e];
+      v = (t >= 0 && t < num_blocks) ? t : blk_first;
     }
-#pragma unroll
-    for (int k = 0; k < LPT; ++k) {
-      const int bb = (k * 256 + wave * 64) / UNITS;  // block of the tile (wave-uniform)
-      const int b = __builtin_amdgcn_readfirstlane(blk[bb]);
-      const size_t base = (size_t)b * hkv * SLAB + head_off;
-      const int ldsoff = (k * 256 + wave * 64) * 8;  // elements; + 8 * lane by the hardware
-      __builtin_amdgcn_global_load_lds(
-          (const void*)(k_cache + base + kofs[k]),
-          (__attribute__((address_space(3))) void*)(&sm.k[buf][ldsoff]), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(
-          (const void*)(v_cache + base + vofs[k]),
-          (__attribute__((address_space(3))) void*)(&sm.v[buf][ldsoff]), 16, 0, 0);
+    return v;
+  };
+  int kchunk = load_chunk(0), kchunk_id = 0;
+  int vchunk = kchunk, vchunk_id = 0;
+  auto block_of = [&](int& chunk, int& chunk_id, int kt) {
+    const int e = kt * 4 + wave;  // this wave's block of tile kt
+    const int c = e >> 6;
+    if (c != chunk_id) {
+      chunk = load_chunk(c);
+      chunk_id = c;
     }
+    return __builtin_amdgcn_readlane(chunk, e & 63);
+  };
+  auto issue = [&](const uint16_t* cache, uint16_t* dst, const int (&ofs)[WLOADS], int blk) {
+    const uint16_t* src = cache + (size_t)blk * hkv * SLAB + head_off;
+#pragma unroll
+    for (int k = 0; k < WLOADS; ++k)
+      __builtin_amdgcn_global_load_lds(
+          (const void*)(src + ofs[k]),
+          (__attribute__((address_space(3))) void*)(dst + wave * SLAB + k * 512), 16, 0, 0);
+  };
+  auto issue_k = [&](int kt, int buf) {
+    issue(k_cache, sm.k[buf], kofs, block_of(kchunk, kchunk_id, kt));
+  };
+  auto issue_v = [&](int kt, int buf) {
+    issue(v_cache, sm.v[buf], vofs, block_of(vchunk, vchunk_id, kt));
   };
 
   // lane-constant LDS read offsets (elements)
   const int kread = (lc >> 4) * SLAB + (hh * 16 + (lc & 15)) * 8;
-  const int vread = (2 * lc + (hh ^ ((lc >> 2) & 1))) * 8;
+  const int vread = (2 * lc + (hh ^ ((lc >> 3) & 1))) * 8;
 
-  issue_tile(0, 0);
-  for (int kt = 0; kt < ntiles; ++kt) {
-    const int buf = kt & 1;
-    wait_vmem();      // this thread's direct loads of tile kt have landed in LDS
-    __syncthreads();  // ... every thread's; and every wave is done reading buffer buf ^ 1
-    if (kt + 1 < ntiles) {
-      issue_tile(kt + 1, buf ^ 1);
-    } else if ((kt + 1) * kKeys > len) {
-      // last tile reaches past the sequence: zero V slots >= len (they may hold any bits)
+  // scores S^T of the K tile in buffer kbuf, both 32-key halves (two independent chains)
+  auto scores = [&](int kbuf, f32x16 (&sc)[2]) {
+    u32x4 ka[2][KK];
 #pragma unroll
-      for (int k = 0; k < 4 * UNITS / 256; ++k) {
+    for (int beta = 0; beta < 2; ++beta)
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk)
+        ka[beta][kk] = ld16(&sm.k[kbuf][kread + beta * 2 * SLAB + kk * 256]);
+#pragma unroll
+    for (int beta = 0; beta < 2; ++beta)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sc[beta][r] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+      for (int beta = 0; beta < 2; ++beta)
+        sc[beta] = mfma32(as_bf16x8(ka[beta][kk]), qf[kk], sc[beta]);
+  };
+
+  // register r of half-tile beta holds the score of key
+  // key0 + 32 beta + 16 (r/8) + 8 hh + 4 ((r/4) % 2) + r % 4
+  auto mask_tile = [&](int key0, f32x16 (&sc)[2]) {
+#pragma unroll
+    for (int beta = 0; beta < 2; ++beta)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = key0 + 32 * beta + 16 * (r >> 3) + 8 * hh + 4 * ((r >> 2) & 1) + (r & 3);
+        sc[beta][r] = key <= lim ? sc[beta][r] : -INFINITY;
+      }
+  };
+
+  // weights of one tile: P = 2^(scale_log2 * S - m) rounded to bf16 (the value-product
+  // operand), and the sum of the rounded weights
+  auto weights = [&](f32x16 (&sc)[2], bf16x8 (&pw)[2][2]) {
+    const float neg_m = -m;
+    float sum = 0.f;
+#pragma unroll
+    for (int beta = 0; beta < 2; ++beta)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        u32x4 w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float a = fast_exp2(__builtin_fmaf(sc[beta][8 * u + 2 * e], scale_log2, neg_m));
+          const float b = fast_exp2(__builtin_fmaf(sc[beta][8 * u + 2 * e + 1], scale_log2, neg_m));
+          w[e] = pack_bf16x2(a, b);
+          sum = add_pair_bf16(w[e], sum);
+        }
+        pw[beta][u] = as_bf16x8(w);
+      }
+    return sum;
+  };
+  // value product of one tile: O^T += V^T P^T; step (beta, u) covers block 2 beta + u of the
+  // tile, lane group hh supplying slots 8 hh .. 8 hh + 7 of V^T row 32 db + lc
+  auto values = [&](int vbuf, const bf16x8 (&pw)[2][2]) {
+    const uint16_t* vt = sm.v[vbuf];
+#pragma unroll
+    for (int beta = 0; beta < 2; ++beta)
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const u32x4 a = ld16(&vt[(2 * beta + u) * SLAB + vread + db * 512]);
+          o[db] = mfma32(as_bf16x8(a), pw[beta][u], o[db]);
+        }
+  };
+
+  // One step of the software pipeline, for tile kt. On entry cur holds the raw scores of
+  // tile kt and pprev the weights of tile kt-1 (when has_prev). One straight-line block
+  // then issues the score MFMAs of tile kt+1 (when has_next) and the value MFMAs of tile
+  // kt-1, interleaved with the softmax of tile kt, whose weights use the running maximum m
+  // speculatively: with the lazy rescale m almost never moves, and when some column's
+  // maximum does grow by more than the threshold (always on the first tile, m = -inf) a
+  // rare branch rescales the accumulator and recomputes the weights.
+  // LDS: step kt reads K(kt+1) from K buffer (kt+1)&1 and V(kt-1) from V buffer (kt-1)&1,
+  // and loads K(kt+2) into K buffer kt&1 and V(kt) into V buffer kt&1 -- the buffers whose
+  // last readers were in step kt-1, which the barrier at the top of step kt has retired.
+  auto step = [&](auto has_prev, auto has_next, int kt, f32x16 (&cur)[2], f32x16 (&nxt)[2],
+                  bf16x8 (&pprev)[2][2], bf16x8 (&pcur)[2][2]) {
+    wait_vmem();
+    __syncthreads();  // K(kt+1) and V(kt-1) have landed; all waves are done with step kt-1
+    if (kt + 2 < ntiles) issue_k(kt + 2, kt & 1);
+    issue_v(kt, kt & 1);
+    if (!wave_live) return;
+    const int key0 = kt * kKeys;
+    if (key0 + kKeys - 1 > p + wj_lo) mask_tile(key0, cur);
+
+    // ---- the straight-line block ----
+    if constexpr (decltype(has_next)::value) scores((kt + 1) & 1, nxt);
+    if constexpr (decltype(has_prev)::value) values((kt - 1) & 1, pprev);
+    float lnew = weights(cur, pcur);
+    // keep the speculative weights in this block: without a use here the compiler would sink
+    // their computation past the rare branch below (which overwrites them), out of reach of
+    // the interleave
+    asm volatile("" ::"v"(__builtin_bit_cast(u32x4, pcur[0][0])),
+                 "v"(__builtin_bit_cast(u32x4, pcur[0][1])),
+                 "v"(__builtin_bit_cast(u32x4, pcur[1][0])),
+                 "v"(__builtin_bit_cast(u32x4, pcur[1][1])), "v"(lnew));
+    float mx4[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int beta = c >> 1, r0 = (c & 1) * 8;
+      mx4[c] = fmaxf(fmaxf(fmaxf(cur[beta][r0], cur[beta][r0 + 1]),
+                           fmaxf(cur[beta][r0 + 2], cur[beta][r0 + 3])),
+                     fmaxf(fmaxf(cur[beta][r0 + 4], cur[beta][r0 + 5]),
+                           fmaxf(cur[beta][r0 + 6], cur[beta][r0 + 7])));
+    }
+    float mx = fmaxf(fmaxf(mx4[0], mx4[1]), fmaxf(mx4[2], mx4[3]));
+    mx = fmaxf(mx, swap_halves(mx)) * scale_log2;
+    const bool grow = mx > m + kRescaleThreshold;
+    if constexpr (decltype(has_next)::value && decltype(has_prev)::value) {
+      // interleave: a few fragment reads ahead, then each of the 32 MFMAs followed by the
+      // next fragment read and a slice of the softmax arithmetic
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);    // 4 LDS reads
+#pragma unroll
+      for (int k = 0; k < 32; ++k) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // 4 VALU
+      }
+    }
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+      const float m_new = grow ? mx : m;
+      const float alpha = fast_exp2(m - m_new);
+      m = m_new;
+      lpart *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+      lnew = weights(cur, pcur);
+    }
+    lpart += lnew;
+  };
+
+  // prologue: K(0) in K buffer 0, then K(1) in flight; scores of tile 0
+  issue_k(0, 0);
+  wait_vmem();
+  __syncthreads();
+  if (ntiles > 1) issue_k(1, 1);
+  f32x16 sa[2], sb[2];
+  bf16x8 pa[2][2], pb[2][2];
+  if (wave_live) scores(0, sa);
+  using yes = std::true_type;
+  using no = std::false_type;
+  // step kt consumes scores sa/sb alternately and writes weights pa/pb alternately
+  if (ntiles == 1) {
+    step(no(), no(), 0, sa, sb, pb, pa);
+  } else {
+    step(no(), yes(), 0, sa, sb, pb, pa);
+    int kt = 1;
+    for (; kt + 2 < ntiles; kt += 2) {
+      step(yes(), yes(), kt, sb, sa, pa, pb);
+      step(yes(), yes(), kt + 1, sa, sb, pb, pa);
+    }
+    if (kt + 1 < ntiles) {
+      step(yes(), yes(), kt, sb, sa, pa, pb);
+      step(yes(), no(), kt + 1, sa, sb, pb, pa);
+      kt += 2;
+    } else {
+      step(yes(), no(), kt, sb, sa, pa, pb);
+      kt += 1;
+    }
+    (void)kt;
+  }
+  // epilogue: V of the last tile (loaded by the last step) lands; where that tile reaches
+  // past the sequence, zero the V slots >= len (they may hold any bits); then its value
+  // product, with the weights in pa when ntiles is odd and in pb when it is even
+  {
+    const int kt = ntiles - 1;
+    wait_vmem();
+    __syncthreads();
+    if ((kt + 1) * kKeys > len) {
+      uint16_t* vt = sm.v[kt & 1];
+#pragma unroll
+      for (int k = 0; k < LPT; ++k) {
         const int P = tid + 256 * k;
         const int bb = P / UNITS, pos = P % UNITS;
         const int d = pos >> 1;
-        const int hf = (pos & 1) ^ ((d >> 2) & 1);
+        const int hf = (pos & 1) ^ ((d >> 3) & 1);
         const int first = kt * kKeys + bb * kBlockSize + hf * 8;
         const int keep = min(max(len - first, 0), 8);
         if (keep < 8) {
-          uint16_t* u = &sm.v[buf][P * 8];
-          u32x4 w = ld16(u);
+          u32x4 w = ld16(&vt[P * 8]);
           uint32_t words[4] = {w[0], w[1], w[2], w[3]};
 #pragma unroll
           for (int e = 0; e < 8; ++e)
             if (e >= keep) words[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
-          st16(u, u32x4{words[0], words[1], words[2], words[3]});
+          st16(&vt[P * 8], u32x4{words[0], words[1], words[2], words[3]});
         }
       }
       __syncthreads();
     }
-
-    const int key0 = kt * kKeys;
-    if (wave_live && key0 <= p + wj_hi) {  // a key of the tile is visible to a wave column
-      // ---- scores S^T (raw): both 32-key halves, as two independent accumulation chains ----
-      u32x4 ka[2][KK];
-#pragma unroll
-      for (int beta = 0; beta < 2; ++beta)
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk)
-          ka[beta][kk] = ld16(&sm.k[buf][kread + beta * 2 * SLAB + kk * 256]);
-      f32x16 s[2];
-#pragma unroll
-      for (int beta = 0; beta < 2; ++beta)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[beta][r] = 0.f;
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk)
-#pragma unroll
-        for (int beta = 0; beta < 2; ++beta)
-          s[beta] = mfma32(as_bf16x8(ka[beta][kk]), qf[kk], s[beta]);
-      // register r of half-tile beta holds the score of key
-      // key0 + 32 beta + 16 (r/8) + 8 hh + 4 ((r/4) % 2) + r % 4
-      if (key0 + kKeys - 1 > p + wj_lo) {
-#pragma unroll
-        for (int beta = 0; beta < 2; ++beta)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = key0 + 32 * beta + 16 * (r >> 3) + 8 * hh + 4 * ((r >> 2) & 1) +
-                            (r & 3);
-            s[beta][r] = key <= lim ? s[beta][r] : -INFINITY;
-          }
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int beta = 0; beta < 2; ++beta)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[beta][r]);
-      mx = fmaxf(mx, swap_halves(mx)) * scale_log2;
-      const bool grow = mx > m + kRescaleThreshold;
-      if (__builtin_amdgcn_ballot_w64(grow)) {
-        const float m_new = grow ? mx : m;
-        const float alpha = fast_exp2(m - m_new);
-        m = m_new;
-        lpart *= alpha;
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-      }
-      const float neg_m = -m;
-      float ps = 0.f;
-      bf16x8 pf[2][2];
-#pragma unroll
-      for (int beta = 0; beta < 2; ++beta)
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          u32x4 w;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float a = fast_exp2(__builtin_fmaf(s[beta][8 * u + 2 * e], scale_log2, neg_m));
-            const float b = fast_exp2(__builtin_fmaf(s[beta][8 * u + 2 * e + 1], scale_log2, neg_m));
-            ps += a + b;
-            w[e] = pack_bf16x2(a, b);
-          }
-          pf[beta][u] = as_bf16x8(w);
-        }
-      lpart += ps;
-      // ---- values: step (beta, u) covers block 2 beta + u of the tile; lane group hh
-      // supplies slots 8 hh .. 8 hh + 7 of V^T row 32 db + lc ----
-#pragma unroll
-      for (int beta = 0; beta < 2; ++beta)
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const uint16_t* vb = &sm.v[buf][(2 * beta + u) * SLAB + vread];
-#pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            const u32x4 a = ld16(vb + db * 512);
-            o[db] = mfma32(as_bf16x8(a), pf[beta][u], o[db]);
-          }
-        }
+    if (wave_live) {
+      if (ntiles & 1) values(kt & 1, pa);
+      else values(kt & 1, pb);
     }
   }
 

@@ -3,7 +3,8 @@
 Argument marshalling only: tensors supply device pointers and torch's current stream supplies
 the hipStream_t; every step of the path runs in the library's HIP kernels. There is no CPU
 fallback: importing this module fails if libpkv.so is missing, and the device calls refuse
-tensors that are not on the GPU."""
+tensors that are not on the GPU. PKV_LIBRARY, if set, names another build of the library
+to load instead of the in-tree one."""
 from __future__ import annotations
 
 import ctypes
@@ -12,7 +13,8 @@ from typing import Optional, Sequence
 
 import numpy as np
 
-_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpkv.so")
+_LIB_PATH = os.environ.get("PKV_LIBRARY") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "libpkv.so")
 
 if not os.path.exists(_LIB_PATH):
     raise ImportError(f"{_LIB_PATH} is missing: build it with "

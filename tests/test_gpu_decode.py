@@ -9,6 +9,7 @@ import oracle
 import workloads as W
 from tests.gpu_util import (DevBatch, bf16_to_f64, compare, dev_pools, i32, say, scale_for,
                             to_host_bits)
+from tests.test_gpu_prefill import LSE_MAX, LSE_MEAN
 
 pytestmark = pytest.mark.gpu
 
@@ -40,7 +41,7 @@ def oracle_decode(case, bi=0):
 
 def check(name, got, ref):
     compare(name + " out", bf16_to_f64(got[0]), ref[0])
-    compare(name + " lse", got[1], ref[1], atol_max=2e-3, atol_mean=2e-4)
+    compare(name + " lse", got[1], ref[1], atol_max=LSE_MAX, atol_mean=LSE_MEAN)
 
 
 @pytest.mark.parametrize("spec", [W.LLAMA3_8B_DECODE.scaled(decode=48),
