@@ -53,6 +53,33 @@ __device__ __forceinline__ u32x2 mask_v4(u32x2 v, int base, int nvalid) {
   return r;
 }
 
+// K and V operands of one 32-key step (two blocks) of one wave, straight from HBM:
+// K: lane (slot col, group grp) holds chunk grp + 4 kk of slot col of each block;
+// V: lane holds slots 4 grp .. 4 grp + 3 of dim row 16 db + col of each block.
+template <int D>
+struct DecodeFrag {
+  u32x4 k[2][D / 32];
+  u32x2 v[2][D / 16];
+};
+
+template <int D>
+__device__ __forceinline__ void decode_load(DecodeFrag<D>& f, const uint16_t* __restrict__ k_cache,
+                                            const uint16_t* __restrict__ v_cache, size_t b0_off,
+                                            size_t b1_off, int col, int grp) {
+#pragma unroll
+  for (int kk = 0; kk < D / 32; ++kk) {
+    const int chunk = grp + 4 * kk;
+    f.k[0][kk] = ld16(k_cache + b0_off + (size_t)(chunk * kBlockSize + col) * 8);
+    f.k[1][kk] = ld16(k_cache + b1_off + (size_t)(chunk * kBlockSize + col) * 8);
+  }
+#pragma unroll
+  for (int db = 0; db < D / 16; ++db) {
+    const int d = db * 16 + col;
+    f.v[0][db] = ld8(v_cache + b0_off + (size_t)d * kBlockSize + 4 * grp);
+    f.v[1][db] = ld8(v_cache + b1_off + (size_t)d * kBlockSize + 4 * grp);
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(256) void decode_partial_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
@@ -91,47 +118,59 @@ __global__ __launch_bounds__(256) void decode_partial_kernel(
     qf[kk] = as_bf16x8(v);
   }
 
+  // The split's blocks (at most 64) in a per-lane register table: lane l holds the pool
+  // offset of the split's block l, or of pool block 0 (a stand-in that is read but masked)
+  // for blocks past the split, past the table or out of the pool. Every load below is then
+  // unconditional, so a step's 24 loads issue back to back and overlap the previous step.
+  const int32_t* table = block_tables + (size_t)i * max_blocks;
+  const int b_first = k0 / kBlockSize;
+  const int nblk = (k1 - k0 + kBlockSize - 1) / kBlockSize;
+  int tab;
+  {
+    const int b = b_first + lane;
+    int e = 0;
+    if (lane < nblk && b < max_blocks) {
+      e = table[b];
+      if (e < 0 || e >= num_blocks) e = 0;
+    }
+    tab = e;
+  }
+  const size_t head_off = (size_t)kvh * SLAB;
+  auto block_off = [&](int step_block) -> size_t {
+    const int e = __builtin_amdgcn_readlane(tab, min(step_block, 63));
+    return (size_t)e * hkv * SLAB + head_off;
+  };
+
   f32x4 acc[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY;
   float lpart = 0.f;
-  const int32_t* table = block_tables + (size_t)i * max_blocks;
-  const size_t head_off = (size_t)kvh * SLAB;
 
-  for (int t0 = k0; t0 < k1; t0 += 32) {
+  auto compute = [&](const DecodeFrag<D>& f, int t0) {
     const int nvalid = min(32, k1 - t0);
-    const int b0 = t0 / kBlockSize;
-    int blk0 = (b0 < max_blocks) ? table[b0] : -1;
-    int blk1 = (nvalid > kBlockSize && b0 + 1 < max_blocks) ? table[b0 + 1] : -1;
-    if (blk0 >= num_blocks) blk0 = -1;
-    if (blk1 >= num_blocks) blk1 = -1;
-    const uint16_t* k0p = k_cache + (size_t)max(blk0, 0) * hkv * SLAB + head_off;
-    const uint16_t* k1p = k_cache + (size_t)max(blk1, 0) * hkv * SLAB + head_off;
-    const uint16_t* v0p = v_cache + (size_t)max(blk0, 0) * hkv * SLAB + head_off;
-    const uint16_t* v1p = v_cache + (size_t)max(blk1, 0) * hkv * SLAB + head_off;
-
-    // scores for the two blocks
     f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      const int chunk = grp + 4 * kk;
-      u32x4 a0 = {0u, 0u, 0u, 0u}, a1 = {0u, 0u, 0u, 0u};
-      if (blk0 >= 0) a0 = ld16(k0p + (size_t)(chunk * kBlockSize + col) * 8);
-      if (blk1 >= 0) a1 = ld16(k1p + (size_t)(chunk * kBlockSize + col) * 8);
-      s0 = mfma16(as_bf16x8(a0), qf[kk], s0);
-      s1 = mfma16(as_bf16x8(a1), qf[kk], s1);
+      s0 = mfma16(as_bf16x8(f.k[0][kk]), qf[kk], s0);
+      s1 = mfma16(as_bf16x8(f.k[1][kk]), qf[kk], s1);
     }
     // lane holds keys 4*grp + r (block 0) and 16 + 4*grp + r (block 1) of column col
     float sv[8];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      sv[r] = (4 * grp + r < nvalid && blk0 >= 0) ? s0[r] * scale_log2 : -INFINITY;
-      sv[4 + r] = (16 + 4 * grp + r < nvalid && blk1 >= 0) ? s1[r] * scale_log2 : -INFINITY;
+      sv[r] = s0[r] * scale_log2;
+      sv[4 + r] = s1[r] * scale_log2;
     }
-    float mx = sv[0];
+    if (nvalid < 32) {
 #pragma unroll
-    for (int r = 1; r < 8; ++r) mx = fmaxf(mx, sv[r]);
+      for (int r = 0; r < 4; ++r) {
+        sv[r] = 4 * grp + r < nvalid ? sv[r] : -INFINITY;
+        sv[4 + r] = 16 + 4 * grp + r < nvalid ? sv[4 + r] : -INFINITY;
+      }
+    }
+    float mx = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
+                     fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
     mx = wave_max16(mx);
     const float m_new = fmaxf(m, mx);
     const float alpha = fast_exp2(m - m_new);
@@ -150,13 +189,9 @@ __global__ __launch_bounds__(256) void decode_partial_kernel(
     pb[2] = pack_bf16x2(pv[4], pv[5]);
     pb[3] = pack_bf16x2(pv[6], pv[7]);
     const bf16x8 pfrag = as_bf16x8(pb);
-
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      const int d = db * 16 + col;
-      u32x2 va = {0u, 0u}, vb = {0u, 0u};
-      if (blk0 >= 0) va = ld8(v0p + (size_t)d * kBlockSize + 4 * grp);
-      if (blk1 >= 0) vb = ld8(v1p + (size_t)d * kBlockSize + 4 * grp);
+      u32x2 va = f.v[0][db], vb = f.v[1][db];
       if (nvalid < 32) {
         va = mask_v4(va, 4 * grp, nvalid);
         vb = mask_v4(vb, 16 + 4 * grp, nvalid);
@@ -167,6 +202,19 @@ __global__ __launch_bounds__(256) void decode_partial_kernel(
       for (int r = 0; r < 4; ++r) c[r] *= alpha;
       acc[db] = mfma16(as_bf16x8(vv), pfrag, c);
     }
+  };
+
+  // two-stage register pipeline: the next step's loads are in flight while this one is
+  // multiplied (the load after the last step reads stand-in blocks and is discarded)
+  DecodeFrag<D> fa, fb;
+  decode_load<D>(fa, k_cache, v_cache, block_off(0), block_off(1), col, grp);
+  for (int t0 = k0, sb = 0;; t0 += 64, sb += 4) {
+    decode_load<D>(fb, k_cache, v_cache, block_off(sb + 2), block_off(sb + 3), col, grp);
+    compute(fa, t0);
+    if (t0 + 32 >= k1) break;
+    decode_load<D>(fa, k_cache, v_cache, block_off(sb + 4), block_off(sb + 5), col, grp);
+    compute(fb, t0 + 32);
+    if (t0 + 64 >= k1) break;
   }
 
   const float l = wave_sum16(lpart);
