@@ -2,8 +2,9 @@
 // context, split along the key axis ("split-K") so that every compute unit streams KV at the
 // HBM rate, followed by a merge of the splits' partial results by their log-sum-exp weights.
 //
-// Work item = (sequence, kv head, split) = one wavefront; a 256-thread workgroup carries four
-// independent work items, so there are no barriers and no LDS. Each wave streams its split
+// Work item = (sequence, kv head, split) = one single-wave workgroup, so a compute unit
+// takes new work as soon as any wave ends (work items differ in length); there are no
+// barriers and no LDS. Each wave streams its split
 // 32 keys (two 16-token blocks) at a time straight from HBM into the matrix-core operands:
 //   scores  S^T[32 keys][16 cols] = K[keys][D] . Q^T[D][cols]      (v_mfma 16x16x32 bf16)
 //   values  O^T[D][16 cols]      += V^T[D][32 keys] . P^T[keys][cols]
@@ -28,7 +29,7 @@
 namespace pkv {
 namespace {
 
-constexpr int kWaves = 4;
+constexpr int kWaves = 4;  // waves per workgroup of the merge kernel
 
 __device__ __forceinline__ float wave_max16(float x) {
   // max over the four lanes l, l^16, l^32, l^48 (the lane groups holding one column)
@@ -66,22 +67,28 @@ template <int D>
 __device__ __forceinline__ void decode_load(DecodeFrag<D>& f, const uint16_t* __restrict__ k_cache,
                                             const uint16_t* __restrict__ v_cache, size_t b0_off,
                                             size_t b1_off, int col, int grp) {
+  // wave-uniform slab bases plus 32-bit per-lane byte offsets
+  constexpr int SLAB_BYTES = D * kBlockSize * 2;
+  const uint16_t* k0 = k_cache + b0_off;
+  const uint16_t* k1 = k_cache + b1_off;
+  const uint16_t* v0 = v_cache + b0_off;
+  const uint16_t* v1 = v_cache + b1_off;
 #pragma unroll
   for (int kk = 0; kk < D / 32; ++kk) {
-    const int chunk = grp + 4 * kk;
-    f.k[0][kk] = ld16(k_cache + b0_off + (size_t)(chunk * kBlockSize + col) * 8);
-    f.k[1][kk] = ld16(k_cache + b1_off + (size_t)(chunk * kBlockSize + col) * 8);
+    const int o = ((grp + 4 * kk) * kBlockSize + col) * 16;
+    f.k[0][kk] = buf_ld16(k0, SLAB_BYTES, o);
+    f.k[1][kk] = buf_ld16(k1, SLAB_BYTES, o);
   }
 #pragma unroll
   for (int db = 0; db < D / 16; ++db) {
-    const int d = db * 16 + col;
-    f.v[0][db] = ld8(v_cache + b0_off + (size_t)d * kBlockSize + 4 * grp);
-    f.v[1][db] = ld8(v_cache + b1_off + (size_t)d * kBlockSize + 4 * grp);
+    const int o = ((db * 16 + col) * kBlockSize + 4 * grp) * 2;
+    f.v[0][db] = buf_ld8(v0, SLAB_BYTES, o);
+    f.v[1][db] = buf_ld8(v1, SLAB_BYTES, o);
   }
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void decode_partial_kernel(
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void decode_partial_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
     const uint16_t* __restrict__ v_cache, const int32_t* __restrict__ block_tables,
     int32_t max_blocks, const int32_t* __restrict__ seq_lens, int32_t num_seqs, int32_t hq,
@@ -95,7 +102,7 @@ __global__ __launch_bounds__(256) void decode_partial_kernel(
   const int lane = threadIdx.x & 63;
   const int col = lane & 15;   // query head within the kv group (column)
   const int grp = lane >> 4;   // lane group 0..3
-  const int64_t item = (int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6);
+  const int64_t item = blockIdx.x;
   const int64_t per_seq = (int64_t)hkv * max_splits;
   const int i = (int)(item / per_seq);
   if (i >= num_seqs) return;
@@ -118,26 +125,32 @@ __global__ __launch_bounds__(256) void decode_partial_kernel(
     qf[kk] = as_bf16x8(v);
   }
 
-  // The split's blocks (at most 64) in a per-lane register table: lane l holds the pool
-  // offset of the split's block l, or of pool block 0 (a stand-in that is read but masked)
-  // for blocks past the split, past the table or out of the pool. Every load below is then
-  // unconditional, so a step's 24 loads issue back to back and overlap the previous step.
+  // The split's blocks in per-lane register tables of 64 entries: chunk c holds, in lane l,
+  // the pool offset of the split's block 64 c + l, or of pool block 0 (a stand-in that is
+  // read but masked) for blocks past the split, past the table or out of the pool. Two
+  // chunks are live (the current one and the next), so every load below is unconditional
+  // and a step's 24 loads issue back to back and overlap the previous step.
   const int32_t* table = block_tables + (size_t)i * max_blocks;
   const int b_first = k0 / kBlockSize;
   const int nblk = (k1 - k0 + kBlockSize - 1) / kBlockSize;
-  int tab;
-  {
-    const int b = b_first + lane;
+  auto load_chunk = [&](int c) -> int {
+    const int r = 64 * c + lane;
+    const int b = b_first + r;
     int e = 0;
-    if (lane < nblk && b < max_blocks) {
+    if (r < nblk && b < max_blocks) {
       e = table[b];
       if (e < 0 || e >= num_blocks) e = 0;
     }
-    tab = e;
-  }
+    return e;
+  };
+  int chunk = 0;
+  int tab = load_chunk(0);
+  int tab_next = load_chunk(1);
   const size_t head_off = (size_t)kvh * SLAB;
-  auto block_off = [&](int step_block) -> size_t {
-    const int e = __builtin_amdgcn_readlane(tab, min(step_block, 63));
+  // block b (0 <= b < 128) counted from the start of the current chunk
+  auto block_off = [&](int b) -> size_t {
+    const int e = b < 64 ? __builtin_amdgcn_readlane(tab, b)
+                         : __builtin_amdgcn_readlane(tab_next, b - 64);
     return (size_t)e * hkv * SLAB + head_off;
   };
 
@@ -209,6 +222,12 @@ __global__ __launch_bounds__(256) void decode_partial_kernel(
   DecodeFrag<D> fa, fb;
   decode_load<D>(fa, k_cache, v_cache, block_off(0), block_off(1), col, grp);
   for (int t0 = k0, sb = 0;; t0 += 64, sb += 4) {
+    if (sb == 64) {  // step into the next chunk of the table
+      sb = 0;
+      ++chunk;
+      tab = tab_next;
+      tab_next = load_chunk(chunk + 1);
+    }
     decode_load<D>(fb, k_cache, v_cache, block_off(sb + 2), block_off(sb + 3), col, grp);
     compute(fa, t0);
     if (t0 + 32 >= k1) break;
@@ -286,10 +305,12 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(
 }  // namespace
 
 int32_t decode_split_keys(int32_t num_seqs, int32_t hkv, int32_t max_seq_len) {
-  // Longest split first; shorten it while the grid would hold too few waves to keep all
-  // 256 compute units streaming (aim for >= 8 waves per unit). A function of the call's
-  // sizes only, so a given call always splits identically.
-  int32_t split = 256;
+  // Longest split first (every split pays a prologue of dependent table and first KV loads
+  // plus a partial write, so fewer, longer splits stream better); shorten it while the grid
+  // would hold too few waves to keep all 256 compute units streaming (aim for >= 8 waves
+  // per unit). A function of the call's sizes only, so a given call always splits
+  // identically.
+  int32_t split = 4096;
   while (split > 64) {
     const int64_t waves =
         (int64_t)num_seqs * hkv * ((max_seq_len + split - 1) / split);
@@ -319,14 +340,14 @@ hipError_t launch_decode(const KvView& kv, const uint16_t* q, int32_t hq,
                      ? nullptr
                      : ws_o + (size_t)num_seqs * hq * max_splits * kv.head_dim;
   const int64_t items = (int64_t)num_seqs * kv.hkv * max_splits;
-  const dim3 grid((unsigned)((items + kWaves - 1) / kWaves));
+  const dim3 grid((unsigned)items);
   const float scale_log2 = scale * kLog2e;
   if (kv.head_dim == 128)
-    hipLaunchKernelGGL(decode_partial_kernel<128>, grid, dim3(256), 0, stream, q, kv.k, kv.v,
+    hipLaunchKernelGGL(decode_partial_kernel<128>, grid, dim3(64), 0, stream, q, kv.k, kv.v,
                        block_tables, max_blocks, seq_lens, num_seqs, hq, kv.hkv,
                        kv.num_blocks, split, max_splits, scale_log2, ws_o, ws_ml, out, lse);
   else
-    hipLaunchKernelGGL(decode_partial_kernel<64>, grid, dim3(256), 0, stream, q, kv.k, kv.v,
+    hipLaunchKernelGGL(decode_partial_kernel<64>, grid, dim3(64), 0, stream, q, kv.k, kv.v,
                        block_tables, max_blocks, seq_lens, num_seqs, hq, kv.hkv,
                        kv.num_blocks, split, max_splits, scale_log2, ws_o, ws_ml, out, lse);
   hipError_t err = hipGetLastError();

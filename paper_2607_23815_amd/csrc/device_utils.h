@@ -50,4 +50,44 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Fourth word of a raw buffer resource on gfx9-family parts: 32-bit data format, no
+// swizzle, no index stride -- a plain byte-addressed buffer.
+constexpr int kBufferFlags = 0x00020000;
+
+// Direct global -> LDS load of 16 bytes per lane through a buffer resource whose base is
+// `base` and which holds `bytes` bytes (the hardware bounds-checks `voffset`): lane i's
+// 16 bytes land at lds + 16 i. The buffer form, unlike the global form, leaves the
+// compiler's LDS-read wait counting exact. The builtins exist for the device target only,
+// so the body is compiled in the device pass.
+__device__ __forceinline__ void lds_load16(const void* base, int bytes, int voffset, void* lds) {
+#if __HIP_DEVICE_COMPILE__
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kBufferFlags);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)lds,
+                                           16, voffset, 0, 0, 0);
+#endif
+}
+
+// 16- and 8-byte loads through a buffer resource: wave-uniform `base` (kept in scalar
+// registers) plus a 32-bit per-lane byte offset, so a load needs one address register
+// instead of two. Offsets at or past `bytes` read zero.
+__device__ __forceinline__ u32x4 buf_ld16(const void* base, int bytes, int voffset) {
+#if __HIP_DEVICE_COMPILE__
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kBufferFlags);
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, voffset, 0, 0));
+#else
+  return u32x4{0u, 0u, 0u, 0u};
+#endif
+}
+__device__ __forceinline__ u32x2 buf_ld8(const void* base, int bytes, int voffset) {
+#if __HIP_DEVICE_COMPILE__
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kBufferFlags);
+  return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rsrc, voffset, 0, 0));
+#else
+  return u32x2{0u, 0u};
+#endif
+}
+
 }  // namespace pkv

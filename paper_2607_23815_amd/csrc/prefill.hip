@@ -70,6 +70,7 @@ struct PrefillSmem {
 // normalisation). After the first tiles the maximum of N(0,1) scores hardly moves, so the
 // 64 accumulator multiplies per tile are almost always skipped.
 constexpr float kRescaleThreshold = 8.0f;
+constexpr float kRescaleLimit = 256.0f;  // 2^kRescaleThreshold
 
 // Sum of the two bf16 values packed in w, added to acc (v_dot2 with (1, 1)).
 __device__ __forceinline__ float add_pair_bf16(uint32_t w, float acc) {
@@ -198,13 +199,12 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
     }
     return __builtin_amdgcn_readlane(chunk, e & 63);
   };
+  // One slab = one buffer resource (base = the slab, 4 KB, bounds-checked by the hardware).
   auto issue = [&](const uint16_t* cache, uint16_t* dst, const int (&ofs)[WLOADS], int blk) {
     const uint16_t* src = cache + (size_t)blk * hkv * SLAB + head_off;
 #pragma unroll
     for (int k = 0; k < WLOADS; ++k)
-      __builtin_amdgcn_global_load_lds(
-          (const void*)(src + ofs[k]),
-          (__attribute__((address_space(3))) void*)(dst + wave * SLAB + k * 512), 16, 0, 0);
+      lds_load16(src, SLAB * 2, ofs[k] * 2, dst + wave * SLAB + k * 512);
   };
   auto issue_k = [&](int kt, int buf) {
     issue(k_cache, sm.k[buf], kofs, block_of(kchunk, kchunk_id, kt));
@@ -249,10 +249,12 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
   };
 
   // weights of one tile: P = 2^(scale_log2 * S - m) rounded to bf16 (the value-product
-  // operand), and the sum of the rounded weights
+  // operand), and the sum of the rounded weights. The sum is kept in four independent
+  // partial sums: a single accumulator would chain 16 dependent adds through the block and
+  // stall the in-order issue that has to keep the matrix cores fed.
   auto weights = [&](f32x16 (&sc)[2], bf16x8 (&pw)[2][2]) {
     const float neg_m = -m;
-    float sum = 0.f;
+    float sum[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int beta = 0; beta < 2; ++beta)
 #pragma unroll
@@ -263,11 +265,12 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
           const float a = fast_exp2(__builtin_fmaf(sc[beta][8 * u + 2 * e], scale_log2, neg_m));
           const float b = fast_exp2(__builtin_fmaf(sc[beta][8 * u + 2 * e + 1], scale_log2, neg_m));
           w[e] = pack_bf16x2(a, b);
-          sum = add_pair_bf16(w[e], sum);
+          // the rounded pair, widened exactly (bf16 -> fp32 is a 16-bit shift)
+          sum[e] += __uint_as_float(w[e] << 16) + __uint_as_float(w[e] & 0xFFFF0000u);
         }
         pw[beta][u] = as_bf16x8(w);
       }
-    return sum;
+    return (sum[0] + sum[1]) + (sum[2] + sum[3]);
   };
   // value product of one tile: O^T += V^T P^T; step (beta, u) covers block 2 beta + u of the
   // tile, lane group hh supplying slots 8 hh .. 8 hh + 7 of V^T row 32 db + lc
@@ -315,22 +318,10 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
                  "v"(__builtin_bit_cast(u32x4, pcur[0][1])),
                  "v"(__builtin_bit_cast(u32x4, pcur[1][0])),
                  "v"(__builtin_bit_cast(u32x4, pcur[1][1])), "v"(lnew));
-    float mx4[4];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int beta = c >> 1, r0 = (c & 1) * 8;
-      mx4[c] = fmaxf(fmaxf(fmaxf(cur[beta][r0], cur[beta][r0 + 1]),
-                           fmaxf(cur[beta][r0 + 2], cur[beta][r0 + 3])),
-                     fmaxf(fmaxf(cur[beta][r0 + 4], cur[beta][r0 + 5]),
-                           fmaxf(cur[beta][r0 + 6], cur[beta][r0 + 7])));
-    }
-    float mx = fmaxf(fmaxf(mx4[0], mx4[1]), fmaxf(mx4[2], mx4[3]));
-    mx = fmaxf(mx, swap_halves(mx)) * scale_log2;
-    const bool grow = mx > m + kRescaleThreshold;
     if constexpr (decltype(has_next)::value && decltype(has_prev)::value) {
-      // interleave: a few fragment reads ahead, then each of the 32 MFMAs followed by the
-      // next fragment read and a slice of the softmax arithmetic
-      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);    // 4 LDS reads
+      // interleave: fragment reads ahead, then each of the 32 MFMAs followed by the next
+      // fragment read and a slice of the softmax arithmetic
+      __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);    // 6 LDS reads
 #pragma unroll
       for (int k = 0; k < 32; ++k) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
@@ -338,16 +329,31 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
         __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // 4 VALU
       }
     }
-    if (__builtin_amdgcn_ballot_w64(grow)) {
-      const float m_new = grow ? mx : m;
-      const float alpha = fast_exp2(m - m_new);
-      m = m_new;
-      lpart *= alpha;
+    // The running maximum only has to move when some weight of the tile exceeds 2^threshold,
+    // and then this lane's (non-negative) weight sum exceeds it too: test the sum, and only
+    // then find the tile's exact maximum (the first tile, where m = -inf, always does).
+    bool check = true;
+    if constexpr (decltype(has_prev)::value)
+      check = __builtin_amdgcn_ballot_w64(!(lnew <= kRescaleLimit)) != 0;
+    if (check) {
+      float mx = -INFINITY;
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
+      for (int beta = 0; beta < 2; ++beta)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-      lnew = weights(cur, pcur);
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, cur[beta][r]);
+      mx = fmaxf(mx, swap_halves(mx)) * scale_log2;
+      const bool grow = mx > m + kRescaleThreshold;
+      if (__builtin_amdgcn_ballot_w64(grow)) {
+        const float m_new = grow ? mx : m;
+        const float alpha = fast_exp2(m - m_new);
+        m = m_new;
+        lpart *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+        lnew = weights(cur, pcur);
+      }
     }
     lpart += lnew;
   };

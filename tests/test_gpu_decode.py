@@ -68,6 +68,20 @@ def test_decode_split_and_block_boundaries(gpu_lib, hq, hkv, d):
     check(spec.name, run_decode(gpu_lib, case), oracle_decode(case))
 
 
+def test_decode_long_contexts_in_long_splits(gpu_lib):
+    """Many sequences keep the grid full, so the split stays long and a split spans several
+    64-block chunks of the block table; a few long contexts cross chunk and split
+    boundaries."""
+    say("[decode] long contexts, long splits")
+    longs = [1023, 1024, 1025, 2049, 4096, 4097, 16383, 16384]
+    ctx = longs + [1 + (7 * j) % 40 for j in range(310)]
+    spec = W.WorkloadSpec("decode_long_splits", 151, 32, 8, 128,
+                          (W.BatchSpec("decode", len(ctx), W.Dist.const(1), W.Dist.const(1)),),
+                          ("scale", 1.25))
+    case = W.make_case(spec, prefix_override=[ctx])
+    check(spec.name, run_decode(gpu_lib, case), oracle_decode(case))
+
+
 def test_decode_small_batch_uses_short_splits(gpu_lib):
     """Few sequences -> the split shrinks to keep the grid full; results must not change
     beyond rounding."""
