@@ -4,11 +4,12 @@
 // the sequence's cached prefix (left in the pool by the upstream operator) followed by the new
 // tokens, all read through the block table. New token j sees keys 0 .. P + j.
 //
-// Work item = (sequence, kv head, tile of 128 query columns). A column is one (new token,
+// Work item = (sequence, kv head, tile of 32 x kWaves query columns). A column is one (new token,
 // query head) pair of the kv head's group, token-major, so the g = Hq/Hkv heads that share
 // the kv head are packed into the matrix-core M dimension and every K/V byte staged in LDS
-// serves all of them. The workgroup has four waves of 32 columns each and walks the keys in
-// tiles of 64 (four 16-token blocks):
+// serves all of them. The workgroup has kWaves waves (4: two independent workgroups per
+// compute unit overlap each other's stalls) of 32 columns each and walks the keys in tiles
+// of 64 (four 16-token blocks):
 //   1. K and V tiles are staged in LDS (double-buffered: the next tile's global loads are in
 //      flight while the current tile is multiplied). Staging is a 16-byte copy of whole pool
 //      slabs with a swizzle on the 16-byte unit index, so the matrix-core operand reads below
@@ -36,7 +37,10 @@
 namespace pkv {
 namespace {
 
-constexpr int kCols = 128;  // query columns per workgroup (4 waves x 32)
+constexpr int kWaves = 4;             // waves per workgroup
+constexpr int kThreads = 64 * kWaves;
+constexpr int kCols = 32 * kWaves;    // query columns per workgroup (32 per wave)
+constexpr int kSlabWaves = kWaves / 4;  // waves staging each of a tile's four block slabs
 constexpr int kKeys = 64;   // keys per tile (4 blocks)
 
 // Wait until every global load this thread issued has completed (vmcnt = 0; the other
@@ -72,15 +76,9 @@ struct PrefillSmem {
 constexpr float kRescaleThreshold = 8.0f;
 constexpr float kRescaleLimit = 256.0f;  // 2^kRescaleThreshold
 
-// Sum of the two bf16 values packed in w, added to acc (v_dot2 with (1, 1)).
-__device__ __forceinline__ float add_pair_bf16(uint32_t w, float acc) {
-  typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
-  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
-  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), one, acc, false);
-}
-
 template <int D>
-__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2)))
+__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads),
+                          amdgpu_waves_per_eu(2, 2)))
 void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
                     const uint16_t* __restrict__ v_cache, const int32_t* __restrict__ block_tables,
                     int32_t max_blocks, const int32_t* __restrict__ cached_lens,
@@ -89,7 +87,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
                     uint16_t* __restrict__ out, float* __restrict__ lse) {
   constexpr int SLAB = D * kBlockSize;
   constexpr int UNITS = SLAB / 8;        // 16-byte units per block slab
-  constexpr int LPT = 4 * UNITS / 256;   // direct loads per thread per tile (K or V)
+  constexpr int LPT = 4 * UNITS / kThreads;  // 16-byte units per thread per tile (K or V)
   constexpr int KK = D / 16;             // k-steps of the score product
   constexpr int DB = D / 32;             // 32-dim blocks of the value product
   __shared__ __align__(16) PrefillSmem<D> sm;
@@ -104,6 +102,12 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
   const int qt = qtiles - 1 - item % qtiles;  // longest (last) query tile first
   const int kvh = (item / qtiles) % hkv;
   const int i = item / (qtiles * hkv);
+
+  // The first table chunk (entry `lane` of the sequence's row, and entry 0) is fetched
+  // before the lengths: its address depends on the sequence only, so the two loads overlap.
+  const int32_t* table = block_tables + (size_t)i * max_blocks;
+  const int32_t t_first = table[0];
+  const int32_t t_lane = (int)(threadIdx.x & 63) < max_blocks ? table[threadIdx.x & 63] : -1;
 
   const int g = hq / hkv;
   const int p = cached_lens[i];
@@ -133,18 +137,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
   const int wj_lo = min(wcol0 / g, n - 1);         // earliest token among the wave's columns
   const bool wave_live = wcol0 < ncols;            // the wave has at least one real column
 
-  // Q as the B operand of S^T = K Q^T: lane holds Q[column lc][16 kk + 8 hh .. +7]
-  bf16x8 qf[KK];
-  {
-    const uint16_t* qrow = q + ((size_t)(row0 + j) * hq + head) * D + hh * 8;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (col_ok) v = ld16(qrow + kk * 16);
-      qf[kk] = as_bf16x8(v);
-    }
-  }
-
+  bf16x8 qf[KK];  // Q fragments, loaded in the prologue
   f32x16 o[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db)
@@ -153,23 +146,24 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
   float m = -INFINITY;
   float lpart = 0.f;
 
-  const int32_t* table = block_tables + (size_t)i * max_blocks;
   const size_t head_off = (size_t)kvh * SLAB;
   // stand-in for blocks past the sequence: its first block (len >= 1, so it owns one)
-  int32_t blk_first = table[0];
-  if (blk_first < 0 || blk_first >= num_blocks) blk_first = 0;
+  const int32_t blk_first = (t_first >= 0 && t_first < num_blocks) ? t_first : 0;
 
-  // ---- staging: direct global -> LDS 16-byte loads. Wave w stages block w of every tile:
-  // its load k fills LDS units 64 k + lane of that block's slab (the whole 4 KB slab at
-  // head_dim 128 in four loads). The bank swizzle is applied on the global side: LDS K unit
+  // ---- staging: direct global -> LDS 16-byte loads. Wave w stages block w % 4 of every
+  // tile, sharing it with the other kWaves / 4 - 1 waves of that block: its load k fills LDS
+  // units 64 (part * WLOADS + k) + lane of that block's slab (with four waves, the whole
+  // 4 KB slab at head_dim 128 in four loads). The bank swizzle is applied on the global side: LDS K unit
   // c*16 + t holds global unit c*16 + swap23(t), LDS V unit 2d + t holds global unit
   // 2d + (t ^ ((d >> 3) & 1)); with these, the 16 lanes the LDS serves per cycle read 16
   // distinct 16-byte bank groups. ----
-  constexpr int WLOADS = UNITS / 64;     // loads per wave per block slab
+  constexpr int WLOADS = UNITS / 64 / kSlabWaves;  // loads per wave per block slab
+  const int slab = wave & 3;                       // the block of the tile this wave stages
+  const int part = wave >> 2;                      // which WLOADS loads of that slab
   int kofs[WLOADS], vofs[WLOADS];        // per-lane element offsets within a block slab
 #pragma unroll
   for (int k = 0; k < WLOADS; ++k) {
-    const int pos = k * 64 + lane;
+    const int pos = (part * WLOADS + k) * 64 + lane;
     const int c = pos >> 4;
     kofs[k] = (c * 16 + swap23(pos & 15)) * 8;
     const int d = pos >> 1;
@@ -188,10 +182,12 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
     }
     return v;
   };
-  int kchunk = load_chunk(0), kchunk_id = 0;
+  int kchunk = (lane * kBlockSize < len && t_lane >= 0 && t_lane < num_blocks) ? t_lane
+                                                                              : blk_first;
+  int kchunk_id = 0;
   int vchunk = kchunk, vchunk_id = 0;
   auto block_of = [&](int& chunk, int& chunk_id, int kt) {
-    const int e = kt * 4 + wave;  // this wave's block of tile kt
+    const int e = kt * 4 + slab;  // the block of tile kt this wave stages
     const int c = e >> 6;
     if (c != chunk_id) {
       chunk = load_chunk(c);
@@ -204,7 +200,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
     const uint16_t* src = cache + (size_t)blk * hkv * SLAB + head_off;
 #pragma unroll
     for (int k = 0; k < WLOADS; ++k)
-      lds_load16(src, SLAB * 2, ofs[k] * 2, dst + wave * SLAB + k * 512);
+      lds_load16(src, SLAB * 2, ofs[k] * 2, dst + slab * SLAB + (part * WLOADS + k) * 512);
   };
   auto issue_k = [&](int kt, int buf) {
     issue(k_cache, sm.k[buf], kofs, block_of(kchunk, kchunk_id, kt));
@@ -249,12 +245,13 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
   };
 
   // weights of one tile: P = 2^(scale_log2 * S - m) rounded to bf16 (the value-product
-  // operand), and the sum of the rounded weights. The sum is kept in four independent
-  // partial sums: a single accumulator would chain 16 dependent adds through the block and
+  // operand), and the sum of the fp32 weights before rounding (each rounded weight is within
+  // a relative 2^-9 of its fp32 value, unbiased). The sum is kept in eight independent
+  // partial sums: a single accumulator would chain dependent adds through the block and
   // stall the in-order issue that has to keep the matrix cores fed.
   auto weights = [&](f32x16 (&sc)[2], bf16x8 (&pw)[2][2]) {
     const float neg_m = -m;
-    float sum[4] = {0.f, 0.f, 0.f, 0.f};
+    float sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int beta = 0; beta < 2; ++beta)
 #pragma unroll
@@ -265,12 +262,12 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
           const float a = fast_exp2(__builtin_fmaf(sc[beta][8 * u + 2 * e], scale_log2, neg_m));
           const float b = fast_exp2(__builtin_fmaf(sc[beta][8 * u + 2 * e + 1], scale_log2, neg_m));
           w[e] = pack_bf16x2(a, b);
-          // the rounded pair, widened exactly (bf16 -> fp32 is a 16-bit shift)
-          sum[e] += __uint_as_float(w[e] << 16) + __uint_as_float(w[e] & 0xFFFF0000u);
+          sum[2 * e] += a;
+          sum[2 * e + 1] += b;
         }
         pw[beta][u] = as_bf16x8(w);
       }
-    return (sum[0] + sum[1]) + (sum[2] + sum[3]);
+    return ((sum[0] + sum[1]) + (sum[2] + sum[3])) + ((sum[4] + sum[5]) + (sum[6] + sum[7]));
   };
   // value product of one tile: O^T += V^T P^T; step (beta, u) covers block 2 beta + u of the
   // tile, lane group hh supplying slots 8 hh .. 8 hh + 7 of V^T row 32 db + lc
@@ -296,13 +293,14 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
   // rare branch rescales the accumulator and recomputes the weights.
   // LDS: step kt reads K(kt+1) from K buffer (kt+1)&1 and V(kt-1) from V buffer (kt-1)&1,
   // and loads K(kt+2) into K buffer kt&1 and V(kt) into V buffer kt&1 -- the buffers whose
-  // last readers were in step kt-1, which the barrier at the top of step kt has retired.
+  // last readers were in step kt-1, which the barrier at the top of step kt has retired
+  // (V(0) is loaded by the prologue, whose buffers are all free).
   auto step = [&](auto has_prev, auto has_next, int kt, f32x16 (&cur)[2], f32x16 (&nxt)[2],
                   bf16x8 (&pprev)[2][2], bf16x8 (&pcur)[2][2]) {
     wait_vmem();
     __syncthreads();  // K(kt+1) and V(kt-1) have landed; all waves are done with step kt-1
     if (kt + 2 < ntiles) issue_k(kt + 2, kt & 1);
-    issue_v(kt, kt & 1);
+    if constexpr (decltype(has_prev)::value) issue_v(kt, kt & 1);  // V(0): prologue
     if (!wave_live) return;
     const int key0 = kt * kKeys;
     if (key0 + kKeys - 1 > p + wj_lo) mask_tile(key0, cur);
@@ -358,11 +356,27 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
     lpart += lnew;
   };
 
-  // prologue: K(0) in K buffer 0, then K(1) in flight; scores of tile 0
-  issue_k(0, 0);
+  // prologue: K(0), K(1) and V(0) (every buffer is free; their blocks are entries 0..7 of
+  // the first chunk), then Q, all under one wait; scores of tile 0
+  issue(k_cache, sm.k[0], kofs, __builtin_amdgcn_readlane(kchunk, slab));
+  if (ntiles > 1) issue(k_cache, sm.k[1], kofs, __builtin_amdgcn_readlane(kchunk, 4 + slab));
+  issue(v_cache, sm.v[0], vofs, __builtin_amdgcn_readlane(kchunk, slab));
+  // Q as the B operand of S^T = K Q^T: lane holds Q[column lc][16 kk + 8 hh .. +7]. A lane
+  // past the last column reads a valid row (token n - 1) and keeps zeros, so the loads are
+  // unconditional and the wait above counts them exactly.
+  {
+    const uint16_t* qrow = q + ((size_t)(row0 + j) * hq + head) * D + hh * 8;
+    u32x4 qv[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) qv[kk] = ld16(qrow + kk * 16);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      const u32x4 zero = {0u, 0u, 0u, 0u};
+      qf[kk] = as_bf16x8(col_ok ? qv[kk] : zero);
+    }
+  }
   wait_vmem();
   __syncthreads();
-  if (ntiles > 1) issue_k(1, 1);
   f32x16 sa[2], sb[2];
   bf16x8 pa[2][2], pb[2][2];
   if (wave_live) scores(0, sa);
@@ -399,7 +413,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
       uint16_t* vt = sm.v[kt & 1];
 #pragma unroll
       for (int k = 0; k < LPT; ++k) {
-        const int P = tid + 256 * k;
+        const int P = tid + kThreads * k;
         const int bb = P / UNITS, pos = P % UNITS;
         const int d = pos >> 1;
         const int hf = (pos & 1) ^ ((d >> 3) & 1);
@@ -452,11 +466,11 @@ hipError_t launch_prefill(const KvView& kv, const uint16_t* q, int32_t hq,
   const dim3 grid((unsigned)items);
   const float scale_log2 = scale * kLog2e;
   if (kv.head_dim == 128)
-    hipLaunchKernelGGL(prefill_kernel<128>, grid, dim3(256), 0, stream, q, kv.k, kv.v,
+    hipLaunchKernelGGL(prefill_kernel<128>, grid, dim3(kThreads), 0, stream, q, kv.k, kv.v,
                        block_tables, max_blocks, cached_lens, cu_new_lens, hq, kv.hkv,
                        kv.num_blocks, (int32_t)qtiles, scale_log2, out, lse);
   else
-    hipLaunchKernelGGL(prefill_kernel<64>, grid, dim3(256), 0, stream, q, kv.k, kv.v,
+    hipLaunchKernelGGL(prefill_kernel<64>, grid, dim3(kThreads), 0, stream, q, kv.k, kv.v,
                        block_tables, max_blocks, cached_lens, cu_new_lens, hq, kv.hkv,
                        kv.num_blocks, (int32_t)qtiles, scale_log2, out, lse);
   return hipGetLastError();
