@@ -82,8 +82,8 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads),
 void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
                     const uint16_t* __restrict__ v_cache, const int32_t* __restrict__ block_tables,
                     int32_t max_blocks, const int32_t* __restrict__ cached_lens,
-                    const int32_t* __restrict__ cu_new_lens, int32_t hq, int32_t hkv,
-                    int32_t num_blocks, int32_t qtiles, float scale_log2,
+                    const int32_t* __restrict__ cu_new_lens, int32_t num_seqs, int32_t hq,
+                    int32_t hkv, int32_t num_blocks, int32_t qtiles, float scale_log2,
                     uint16_t* __restrict__ out, float* __restrict__ lse) {
   constexpr int SLAB = D * kBlockSize;
   constexpr int UNITS = SLAB / 8;        // 16-byte units per block slab
@@ -92,16 +92,18 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
   constexpr int DB = D / 32;             // 32-dim blocks of the value product
   __shared__ __align__(16) PrefillSmem<D> sm;
 
-  // XCD-aware mapping: consecutive workgroup ids go to different XCDs (id % 8), so give each
-  // XCD a contiguous range of work items; the query tiles of one (sequence, kv head), which
-  // all read the same K/V, then run on one XCD and share its L2.
-  const int nwg = gridDim.x;
-  const int lin = blockIdx.x;
-  const int xcd = lin & 7;
-  const int item = xcd * (nwg >> 3) + min(xcd, nwg & 7) + (lin >> 3);
-  const int qt = qtiles - 1 - item % qtiles;  // longest (last) query tile first
-  const int kvh = (item / qtiles) % hkv;
-  const int i = item / (qtiles * hkv);
+  // XCD-aware mapping: workgroup id b runs on XCD b % 8. The unit that must stay on one XCD
+  // is a (sequence, kv head) group -- its query tiles read the same K/V and share that XCD's
+  // L2 when they run together -- so groups are dealt to XCDs round-robin (group index mod 8)
+  // and each XCD walks its groups in order, query tiles longest first. With 8 kv heads every
+  // XCD receives one kv head of every sequence: equal work per XCD, whatever the lengths.
+  const int xcd = blockIdx.x & 7;
+  const int pos = blockIdx.x >> 3;                 // position in this XCD's list
+  const int group = (pos / qtiles) * 8 + xcd;      // (sequence, kv head) group index
+  const int qt = qtiles - 1 - pos % qtiles;        // longest (last) query tile first
+  if (group >= num_seqs * hkv) return;
+  const int kvh = group % hkv;
+  const int i = group / hkv;
 
   // The first table chunk (entry `lane` of the sequence's row, and entry 0) is fetched
   // before the lengths: its address depends on the sequence only, so the two loads overlap.
@@ -461,17 +463,18 @@ hipError_t launch_prefill(const KvView& kv, const uint16_t* q, int32_t hq,
                           float* lse, hipStream_t stream) {
   const int32_t g = hq / kv.hkv;
   const int64_t qtiles = ((int64_t)max_new_len * g + kCols - 1) / kCols;
-  const int64_t items = qtiles * kv.hkv * num_seqs;
+  const int64_t groups = (int64_t)kv.hkv * num_seqs;
+  const int64_t items = (groups + 7) / 8 * 8 * qtiles;  // 8 XCD lists of equal length
   if (items > INT32_MAX) return hipErrorInvalidValue;
   const dim3 grid((unsigned)items);
   const float scale_log2 = scale * kLog2e;
   if (kv.head_dim == 128)
     hipLaunchKernelGGL(prefill_kernel<128>, grid, dim3(kThreads), 0, stream, q, kv.k, kv.v,
-                       block_tables, max_blocks, cached_lens, cu_new_lens, hq, kv.hkv,
+                       block_tables, max_blocks, cached_lens, cu_new_lens, num_seqs, hq, kv.hkv,
                        kv.num_blocks, (int32_t)qtiles, scale_log2, out, lse);
   else
     hipLaunchKernelGGL(prefill_kernel<64>, grid, dim3(kThreads), 0, stream, q, kv.k, kv.v,
-                       block_tables, max_blocks, cached_lens, cu_new_lens, hq, kv.hkv,
+                       block_tables, max_blocks, cached_lens, cu_new_lens, num_seqs, hq, kv.hkv,
                        kv.num_blocks, (int32_t)qtiles, scale_log2, out, lse);
   return hipGetLastError();
 }
