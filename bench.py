@@ -433,6 +433,66 @@ def secondary(args, lib, torch):
     return out
 
 
+def reuse_vs_recompute(args, lib, torch):
+    """Kernel-level analog of the paper's prefix reuse (Section 2.1): one downstream attention
+    layer with the cached prefix reused (append the N new tokens, prefill them over P cached
+    ones) against the same layer recomputed from scratch (append all P + N tokens, prefill all
+    of them), on the same data. The recompute runs first: its append places every token's
+    K/V, which the reuse step then reads as its cache."""
+    import workloads as W
+    from tests.gpu_util import i32
+    stream = torch.cuda.current_stream()
+    steps, warm = max(5, args.steps // 2), 2
+
+    def one(spec):
+        b0 = W.plan_case(spec).batches[0]
+        P = b0.prefix_lens.astype(np.int64)
+        N = b0.new_lens.astype(np.int64)
+        L = P + N
+        case = W.plan_case(spec, prefix_override=[np.zeros_like(L)], new_override=[L])
+        W.fill_device(case, "cuda")
+        b = case.batches[0]
+        hq, hkv, d = spec.num_q_heads, spec.num_kv_heads, spec.head_dim
+        scale = 1.0 / math.sqrt(d)
+        pk, pv = case.pool_k, case.pool_v
+        tables = i32(b.block_tables)
+        zeros = i32(np.zeros(len(L)))
+        cu_r = b.cu_new_lens.astype(np.int64)
+        suf = torch.from_numpy(np.concatenate(
+            [np.arange(cu_r[i] + P[i], cu_r[i + 1]) for i in range(len(L))])).cuda()
+        qs, ks, vs = b.q[suf].contiguous(), b.k_new[suf].contiguous(), b.v_new[suf].contiguous()
+        cu_l, cu_n, cached = i32(cu_r), i32(np.concatenate([[0], np.cumsum(N)])), i32(P)
+        maxl, maxn = int(L.max()), int(N.max())
+        o_r = torch.empty((int(L.sum()), hq, d), dtype=torch.bfloat16, device="cuda")
+        o_u = torch.empty((int(N.sum()), hq, d), dtype=torch.bfloat16, device="cuda")
+        recompute = [lambda: lib.pkv_kv_append(pk, pv, b.k_new, b.v_new, tables, zeros, cu_l,
+                                               maxl),
+                     lambda: lib.pkv_prefill_attention(pk, pv, b.q, tables, zeros, cu_l, maxl,
+                                                       maxl, scale, o_r)]
+        reuse = [lambda: lib.pkv_kv_append(pk, pv, ks, vs, tables, cached, cu_n, maxn),
+                 lambda: lib.pkv_prefill_attention(pk, pv, qs, tables, cached, cu_n, maxn, maxl,
+                                                   scale, o_u)]
+        _, g_r, per_r = time_events(torch, stream, recompute, steps, warm)
+        _, g_u, per_u = time_events(torch, stream, reuse, steps, warm)
+        f_r = prefill_flops(np.zeros_like(L), L, hq, d)
+        f_u = prefill_flops(P, N, hq, d)
+        res = {"tuples": int(len(L)), "mean_prefix": float(P.mean()), "mean_new": float(N.mean()),
+               "reuse_ms": g_u * 1e3, "recompute_ms": g_r * 1e3, "speedup": g_r / g_u,
+               "reuse_prefill_TFLOP_s": f_u / per_u[1] / 1e12,
+               "recompute_prefill_TFLOP_s": f_r / per_r[1] / 1e12}
+        del case, pk, pv, o_r, o_u, qs, ks, vs
+        torch.cuda.empty_cache()
+        return res
+
+    out = {W.LLAMA3_8B_PREFILL.name: one(W.LLAMA3_8B_PREFILL)}
+    for k, p in enumerate((256, 1024, 4096)):
+        spec = W.WorkloadSpec(f"prefix_{p}_new_128", 210 + k, 32, 8, 128,
+                              (W.BatchSpec("prefill", 64, W.Dist.const(p), W.Dist.const(128)),),
+                              ("scale", 1.25))
+        out[spec.name] = one(spec)
+    return out
+
+
 def profile_copy(args, torch):
     """A plain device copy of known size (1 GiB read + 1 GiB written per launch): the
     reference that scales the L2<->HBM byte counters to bytes."""
@@ -525,6 +585,7 @@ def main():
     if not args.no_secondary:
         log("[bench] secondary workloads ...")
         res["secondary"] = secondary(args, lib, torch)
+        res["secondary"]["reuse_vs_recompute"] = reuse_vs_recompute(args, lib, torch)
         log("[bench] secondary done")
     print(json.dumps(res), flush=True)
 

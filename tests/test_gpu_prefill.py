@@ -14,9 +14,9 @@ from tests.gpu_util import (DevBatch, bf16_to_f64, compare, dev_pools, say, scal
 
 pytestmark = pytest.mark.gpu
 
-# The kernel sums the bf16-rounded weights (the same values the value product uses), each
-# within a relative 2^-9 of the exact weight, so ln(sum) is within 2^-9 ~ 1.95e-3 of the
-# exact log-sum-exp (plus fp32 rounding of the scores, ~1e-5).
+# The kernel sums the fp32 weights; the bf16 weights the value product uses are each within
+# a relative 2^-9 of those, so the normalisation and ln(sum) are within 2^-9 ~ 1.95e-3 of the
+# exact log-sum-exp in the worst case (plus fp32 rounding of the scores, ~1e-5).
 LSE_MAX = 2.5e-3
 LSE_MEAN = 5e-4
 
