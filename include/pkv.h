@@ -173,7 +173,10 @@ size_t pkv_prefill_workspace_bytes(int32_t num_seqs, int32_t total_new, int32_t 
  * writes a partial result to the workspace and a second kernel merges them with their
  * log-sum-exp weights. q, out: bf16 [num_seqs][num_q_heads][head_dim]; lse: float
  * [num_seqs][num_q_heads] or NULL; seq_lens: int32 [num_seqs], each >= 1. max_seq_len (host)
- * >= every seq_lens[i]. workspace: device memory of at least pkv_decode_workspace_bytes. */
+ * >= every seq_lens[i]. workspace: device memory of at least pkv_decode_workspace_bytes
+ * (non-zero whenever num_seqs > 0: it also holds the order in which sequences are
+ * scheduled, longest first), 16-byte aligned, owned by the caller, not read back; calls
+ * that share a workspace must not overlap. */
 pkv_status pkv_decode_attention(const pkv_paged_kv* kv, const void* q, int32_t num_q_heads,
                                 const int32_t* block_tables, int32_t max_blocks,
                                 const int32_t* seq_lens, int32_t num_seqs, int32_t max_seq_len,

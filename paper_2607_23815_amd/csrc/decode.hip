@@ -4,7 +4,8 @@
 //
 // Work item = (sequence, kv head, split) = one single-wave workgroup, so a compute unit
 // takes new work as soon as any wave ends (work items differ in length); there are no
-// barriers and no LDS. Each wave streams its split
+// barriers and no LDS. Sequences are taken longest first (a small ordering kernel runs
+// before the launch), so the launch does not end on a few long waves. Each wave streams its split
 // 32 keys (two 16-token blocks) at a time straight from HBM into the matrix-core operands:
 //   scores  S^T[32 keys][16 cols] = K[keys][D] . Q^T[D][cols]      (v_mfma 16x16x32 bf16)
 //   values  O^T[D][16 cols]      += V^T[D][32 keys] . P^T[keys][cols]
@@ -94,7 +95,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     int32_t max_blocks, const int32_t* __restrict__ seq_lens, int32_t num_seqs, int32_t hq,
     int32_t hkv, int32_t num_blocks, int32_t split_keys, int32_t max_splits, float scale_log2,
     float* __restrict__ ws_o, float* __restrict__ ws_ml, uint16_t* __restrict__ out,
-    float* __restrict__ lse) {
+    float* __restrict__ lse, const int32_t* __restrict__ order) {
   constexpr int KK = D / 32;   // k-steps of the score product
   constexpr int DB = D / 16;   // 16-dim blocks of the value product
   constexpr int SLAB = D * kBlockSize;
@@ -104,8 +105,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   const int grp = lane >> 4;   // lane group 0..3
   const int64_t item = blockIdx.x;
   const int64_t per_seq = (int64_t)hkv * max_splits;
-  const int i = (int)(item / per_seq);
-  if (i >= num_seqs) return;
+  const int rank = (int)(item / per_seq);
+  if (rank >= num_seqs) return;
+  const int i = order[rank];  // longest sequences first
   const int rem = (int)(item % per_seq);
   const int kvh = rem / max_splits;
   const int sp = rem % max_splits;
@@ -302,6 +304,50 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(
   if (lse != nullptr && lane == 0) lse[item] = (mmax + log2f(den)) * kLn2;
 }
 
+// Longest-first sequence order for the decode grid: waves are dispatched in item order, so
+// taking the longest sequences first keeps the launch from ending on a few long waves.
+// Sequences are bucketed by length on a log scale (32 buckets per factor of two), counted,
+// scanned in descending bucket order and scattered; order within a bucket follows the
+// scatter's atomics and may differ from run to run, which the results do not depend on.
+constexpr int kOrderBuckets = 2048;
+constexpr int kOrderThreads = 1024;
+__global__ __launch_bounds__(kOrderThreads) void decode_order_kernel(
+    const int32_t* __restrict__ seq_lens, int32_t num_seqs, int32_t* __restrict__ order) {
+  __shared__ int count[kOrderBuckets];
+  __shared__ int base[kOrderBuckets];
+  __shared__ int part[kOrderThreads];
+  const int t = threadIdx.x;
+  for (int b = t; b < kOrderBuckets; b += kOrderThreads) count[b] = 0;
+  __syncthreads();
+  auto bucket_of = [&](int i) {
+    const int len = seq_lens[i];
+    if (len < 1) return 0;
+    return min(1 + (int)(log2f((float)len) * 32.f), kOrderBuckets - 1);
+  };
+  for (int i = t; i < num_seqs; i += kOrderThreads) atomicAdd(&count[bucket_of(i)], 1);
+  __syncthreads();
+  // exclusive scan in descending bucket order: thread t owns descending positions 2t, 2t+1
+  const int b0 = kOrderBuckets - 1 - 2 * t, b1 = b0 - 1;
+  const int c0 = count[b0], c1 = count[b1];
+  part[t] = c0 + c1;
+  __syncthreads();
+  for (int off = 1; off < kOrderThreads; off <<= 1) {
+    const int v = t >= off ? part[t - off] : 0;
+    __syncthreads();
+    part[t] += v;
+    __syncthreads();
+  }
+  const int excl = part[t] - (c0 + c1);
+  base[b0] = excl;
+  base[b1] = excl + c0;
+  __syncthreads();
+  for (int i = t; i < num_seqs; i += kOrderThreads) order[atomicAdd(&base[bucket_of(i)], 1)] = i;
+}
+
+size_t order_bytes(int32_t num_seqs) {
+  return ((size_t)num_seqs * sizeof(int32_t) + 255) / 256 * 256;
+}
+
 }  // namespace
 
 int32_t decode_split_keys(int32_t num_seqs, int32_t hkv, int32_t max_seq_len) {
@@ -324,8 +370,10 @@ size_t decode_workspace_bytes(int32_t num_seqs, int32_t hq, int32_t hkv, int32_t
                               int32_t max_seq_len) {
   const int32_t split = decode_split_keys(num_seqs, hkv, max_seq_len);
   const int64_t max_splits = (max_seq_len + split - 1) / split;
-  if (max_splits <= 1) return 0;
-  return (size_t)num_seqs * hq * max_splits * (head_dim + 2) * sizeof(float);
+  // the sequence order, then (when sequences split) the partial results
+  size_t bytes = order_bytes(num_seqs);
+  if (max_splits > 1) bytes += (size_t)num_seqs * hq * max_splits * (head_dim + 2) * sizeof(float);
+  return bytes;
 }
 
 hipError_t launch_decode(const KvView& kv, const uint16_t* q, int32_t hq,
@@ -335,22 +383,31 @@ hipError_t launch_decode(const KvView& kv, const uint16_t* q, int32_t hq,
                          hipStream_t stream) {
   const int32_t split = decode_split_keys(num_seqs, kv.hkv, max_seq_len);
   const int32_t max_splits = (max_seq_len + split - 1) / split;
-  float* ws_o = static_cast<float*>(workspace);
-  float* ws_ml = ws_o == nullptr
-                     ? nullptr
-                     : ws_o + (size_t)num_seqs * hq * max_splits * kv.head_dim;
+  int32_t* order = static_cast<int32_t*>(workspace);
+  float* ws_o = nullptr;
+  float* ws_ml = nullptr;
+  if (max_splits > 1) {
+    ws_o = reinterpret_cast<float*>(static_cast<char*>(workspace) + order_bytes(num_seqs));
+    ws_ml = ws_o + (size_t)num_seqs * hq * max_splits * kv.head_dim;
+  }
   const int64_t items = (int64_t)num_seqs * kv.hkv * max_splits;
   const dim3 grid((unsigned)items);
   const float scale_log2 = scale * kLog2e;
+  hipLaunchKernelGGL(decode_order_kernel, dim3(1), dim3(kOrderThreads), 0, stream, seq_lens,
+                     num_seqs, order);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
   if (kv.head_dim == 128)
     hipLaunchKernelGGL(decode_partial_kernel<128>, grid, dim3(64), 0, stream, q, kv.k, kv.v,
                        block_tables, max_blocks, seq_lens, num_seqs, hq, kv.hkv,
-                       kv.num_blocks, split, max_splits, scale_log2, ws_o, ws_ml, out, lse);
+                       kv.num_blocks, split, max_splits, scale_log2, ws_o, ws_ml, out, lse,
+                       order);
   else
     hipLaunchKernelGGL(decode_partial_kernel<64>, grid, dim3(64), 0, stream, q, kv.k, kv.v,
                        block_tables, max_blocks, seq_lens, num_seqs, hq, kv.hkv,
-                       kv.num_blocks, split, max_splits, scale_log2, ws_o, ws_ml, out, lse);
-  hipError_t err = hipGetLastError();
+                       kv.num_blocks, split, max_splits, scale_log2, ws_o, ws_ml, out, lse,
+                       order);
+  err = hipGetLastError();
   if (err != hipSuccess || max_splits <= 1) return err;
   const int64_t rows = (int64_t)num_seqs * hq;
   const dim3 mgrid((unsigned)((rows + kWaves - 1) / kWaves));

@@ -256,6 +256,9 @@ def pkv_decode_attention(k_cache, v_cache, q, block_tables, seq_lens, max_seq_le
     import torch
     kv = paged_kv(k_cache, v_cache)
     b, hq, d = q.shape
+    if workspace is None:  # convenience for one-off calls; timed callers pass their own
+        workspace = alloc_workspace(pkv_decode_workspace_bytes(b, hq, int(k_cache.shape[1]), d,
+                                                               int(max_seq_len)))
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(_lib.pkv_decode_attention(
         ctypes.byref(kv), _dev_ptr(q, "q", torch.bfloat16), hq,

@@ -204,6 +204,7 @@ def test_device_calls_validate_on_the_host(lib):
 def test_decode_workspace_is_a_function_of_sizes(lib):
     a = lib.pkv_decode_workspace_bytes(512, 32, 8, 128, 2049)
     assert a == lib.pkv_decode_workspace_bytes(512, 32, 8, 128, 2049)
-    # one split -> no workspace
-    assert lib.pkv_decode_workspace_bytes(4096, 32, 8, 128, 60) == 0
+    # one split -> only the longest-first sequence order (int32 per sequence, 256-byte rounded)
+    assert lib.pkv_decode_workspace_bytes(4096, 32, 8, 128, 60) == 4096 * 4
+    assert lib.pkv_decode_workspace_bytes(3, 32, 8, 128, 60) == 256
     assert lib.pkv_prefill_workspace_bytes(256, 40000, 32, 8, 128, 256, 1280) == 0
