@@ -27,7 +27,7 @@ Every function here is pinned by `-m "not gpu"` tests in tests/test_oracle_pins.
 tests/test_block_pool_model.py (library routines, closed forms, invariants, brute force).
 """
 from .bf16 import bf16_bits_to_f64, bf16_bits_to_f32
-from .paged import gather_seq, gather_kv, kv_append
+from .paged import gather_seq, gather_kv, kv_append, copy_blocks
 from .attention import softmax_attention, prefill_attention, decode_attention
 from .block_pool import BlockPoolModel, Status
 from .sizes import kv_bytes_per_token

@@ -70,3 +70,20 @@ def kv_append(pool_k, pool_v, block_tables, cached_lens, cu_new_lens, k_new, v_n
             pk[blk, :, :, slot, :] = np.asarray(k_new[a + j]).reshape(hkv, nchunk, e)
             pv[blk, :, :, slot] = v_new[a + j]
     return pk, pv
+
+
+def copy_blocks(pool_k, pool_v, pairs):
+    """Copy-on-write's device half: return copies of the pools in which block `dst` holds
+    block `src`'s K and V (every kv head, every slot) for each (src, dst) in pairs. Sources are
+    read from the pools as given (no pair sees another's copy). A pair naming a block outside
+    the pool is skipped, as the library documents."""
+    pk = np.array(pool_k, copy=True)
+    pv = np.array(pool_v, copy=True)
+    nb = pk.shape[0]
+    for src, dst in pairs:
+        src, dst = int(src), int(dst)
+        if not (0 <= src < nb and 0 <= dst < nb):
+            continue
+        pk[dst] = pool_k[src]
+        pv[dst] = pool_v[src]
+    return pk, pv
