@@ -57,7 +57,8 @@ typedef enum {
   PKV_ERR_SHARED_BLOCK_WRITE = 3, /* reserve refused: the write range hits a shared block */
   PKV_ERR_UNSUPPORTED_SHAPE = 4,  /* block_size / head_dim / head ratio not supported */
   PKV_ERR_NOT_FOUND = 5,          /* unknown sequence id */
-  PKV_ERR_HIP = 6                 /* a HIP runtime call or launch failed */
+  PKV_ERR_HIP = 6,                /* a HIP runtime call or launch failed */
+  PKV_ERR_KEY_EXISTS = 7          /* prefix publish refused: the key is already cached */
 } pkv_status;
 
 /* Message of this thread's last failed call ("" if none). */
@@ -94,9 +95,11 @@ pkv_status pkv_seq_create(pkv_pool* pool, int64_t* seq_id);
 pkv_status pkv_seq_fork(pkv_pool* pool, int64_t parent, int32_t shared_tokens, int64_t* child);
 
 /* Reserve room for new_tokens more tokens after the sequence's committed and already
- * reserved tokens. All-or-nothing: OUT_OF_BLOCKS when too few blocks are free and
- * SHARED_BLOCK_WRITE when the range would write into a block held by another sequence; in
- * both cases nothing changes. Blocks come from the front of the free list, in order. */
+ * reserved tokens. When too few blocks are free, idle unpinned cached prefixes are evicted
+ * first (see the prefix cache below). All-or-nothing: OUT_OF_BLOCKS when even eviction
+ * cannot free enough blocks and SHARED_BLOCK_WRITE when the range would write into a block
+ * held by another sequence or a cached prefix; in both cases nothing changes (no eviction
+ * either). Blocks come from the front of the free list, in order. */
 pkv_status pkv_seq_reserve(pkv_pool* pool, int64_t seq, int32_t new_tokens);
 
 /* Mark new_tokens reserved tokens as written (after kv_append); 0 <= new_tokens <= reserved. */
@@ -108,6 +111,84 @@ pkv_status pkv_seq_free(pkv_pool* pool, int64_t seq);
 
 /* Committed length of a sequence. */
 pkv_status pkv_seq_len(const pkv_pool* pool, int64_t seq, int32_t* len);
+
+/* ---------------------------------------------------------------------------------------
+ * Prefix cache, eviction and pinning (the allocator side of Section 6).
+ *
+ * Section 2.1 (automatic prefix caching): the KV of an identical prefix is reused and only
+ * the new suffix computed; the reuse is opportunistic because a finished request's blocks
+ * can be reclaimed. A sequence publishes its first `tokens` committed tokens under a 64-bit
+ * key chosen by the caller (e.g. a hash of the tuple's prompt tokens). The entry holds one
+ * reference on each of the ceil(tokens / block_size) blocks, so they stay resident after the
+ * sequence is freed; attach turns a hit into a new sequence that shares them.
+ *
+ * Eviction: when a reservation (pkv_seq_reserve / pkv_seq_reserve_cow) finds too few free
+ * blocks, entries are dropped in policy order until enough are free, all-or-nothing like
+ * the reservation itself. Policy (Section 3 weighs both): least recently used first
+ * (default) or most recently used first, by a logical clock that each publish and each hit
+ * advances. Only idle entries are candidates: no sequence holds any of their blocks. A block
+ * returns to the back of the free list when its last holder (sequence or entry) lets go.
+ *
+ * Pinning (Section 6): under explicit pinning (default) an entry whose pin count is positive
+ * is never evicted until it is unpinned; under virtual pinning pins protect nothing and the
+ * eviction order alone decides. Pin counts are kept in both modes. Deadlock check
+ * (Section 6): requests waiting while none runs means the pipeline is stuck on pinned
+ * memory; recovery unpins every entry and switches to virtual pinning.
+ * --------------------------------------------------------------------------------------- */
+enum { PKV_EVICT_LRU = 0, PKV_EVICT_MRU = 1 };
+enum { PKV_PIN_EXPLICIT = 0, PKV_PIN_VIRTUAL = 1 };
+
+pkv_status pkv_pool_set_eviction(pkv_pool* pool, int32_t policy); /* PKV_EVICT_* */
+pkv_status pkv_pool_set_pinning(pkv_pool* pool, int32_t mode);    /* PKV_PIN_* */
+
+/* Deadlock hook, to be polled with the serving engine's queue state: if waiting > 0 and
+ * running == 0, every entry's pin count is set to zero and pinning becomes virtual
+ * (*recovered = 1); otherwise nothing changes (*recovered = 0). The caller may switch back
+ * to explicit pinning with pkv_pool_set_pinning once the pipeline drains. */
+pkv_status pkv_pool_check_deadlock(pkv_pool* pool, int32_t waiting, int32_t running,
+                                   int32_t* recovered);
+
+/* Publish the first tokens (1 <= tokens <= committed length) of seq under key; KEY_EXISTS
+ * if the key is cached already (nothing changes). The last block may be partly filled: the
+ * publishing sequence then shares it, and writing further into it needs
+ * pkv_seq_reserve_cow. */
+pkv_status pkv_prefix_publish(pkv_pool* pool, int64_t seq, uint64_t key, int32_t tokens);
+
+/* Look the key up. Hit: a new sequence (*seq) shares the entry's blocks, its committed
+ * length is the entry's token count (*tokens), and the entry becomes most recently used.
+ * Miss: NOT_FOUND, and nothing changes but the miss count. */
+pkv_status pkv_prefix_attach(pkv_pool* pool, uint64_t key, int64_t* seq, int32_t* tokens);
+
+/* Pin counts of an entry (NOT_FOUND for an unknown key; unpin of an unpinned entry is
+ * INVALID_ARG). */
+pkv_status pkv_prefix_pin(pkv_pool* pool, uint64_t key);
+pkv_status pkv_prefix_unpin(pkv_pool* pool, uint64_t key);
+
+/* Drop an entry now, whatever its pins (the scheduler knows no task will reuse it). */
+pkv_status pkv_prefix_release(pkv_pool* pool, uint64_t key);
+
+/* Copy-on-write reservation: as pkv_seq_reserve, but each block of the write range that
+ * another holder shares is replaced in the sequence's table by a fresh private block (taken
+ * from the free list before the blocks the growth needs; eviction counts both). The pairs
+ * (source block, copy) go to copies[2k], copies[2k+1] (host, room for max_copies pairs),
+ * *num_copies receives their number; before appending, the caller copies those blocks'
+ * contents on the device (pkv_copy_blocks). INVALID_ARG if more than max_copies copies are
+ * needed; on any refusal nothing changes and *num_copies is 0. */
+pkv_status pkv_seq_reserve_cow(pkv_pool* pool, int64_t seq, int32_t new_tokens, int32_t* copies,
+                               int32_t max_copies, int32_t* num_copies);
+
+typedef struct {
+  int32_t num_free;        /* blocks on the free list */
+  int32_t num_entries;     /* cached prefixes */
+  int32_t cached_blocks;   /* blocks held only by cached prefixes (evictable if unpinned) */
+  int32_t pinned_entries;  /* entries with a positive pin count */
+  int32_t eviction;        /* PKV_EVICT_* */
+  int32_t pinning;         /* PKV_PIN_* */
+  int64_t hits, misses;    /* attach outcomes */
+  int64_t evictions;       /* entries dropped by reservations */
+  int64_t cow_copies;      /* blocks copied on write */
+} pkv_pool_stats;
+pkv_status pkv_pool_get_stats(const pkv_pool* pool, pkv_pool_stats* out);
 
 /* Export block tables: host_tables [n][max_blocks] receives each sequence's physical block
  * ids (reserved blocks included), padded with -1; host_lens [n] (may be NULL) receives the
@@ -184,6 +265,14 @@ pkv_status pkv_decode_attention(const pkv_paged_kv* kv, const void* q, int32_t n
                                 size_t workspace_bytes, void* stream);
 size_t pkv_decode_workspace_bytes(int32_t num_seqs, int32_t num_q_heads, int32_t num_kv_heads,
                                   int32_t head_dim, int32_t max_seq_len);
+
+/* Block copy (the device half of copy-on-write): for each k < num_pairs, the K and V of
+ * every kv head in block pairs[2k] are copied bit-exactly into block pairs[2k+1]. pairs:
+ * int32 device memory [num_pairs][2], e.g. the pairs pkv_seq_reserve_cow returned; every
+ * copy must be distinct from every other block named in the call (the copies run
+ * concurrently). A pair naming a block outside 0..num_blocks-1 is skipped. */
+pkv_status pkv_copy_blocks(const pkv_paged_kv* kv, const int32_t* pairs, int32_t num_pairs,
+                           void* stream);
 
 /* Paged gather (test support): copies the first lens[i] tokens of every sequence out of the
  * pool into contiguous k_out / v_out, bf16 [sum lens][num_kv_heads][head_dim], sequence i

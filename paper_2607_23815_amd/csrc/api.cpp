@@ -26,6 +26,7 @@ pkv_status ok() {
 namespace {
 
 constexpr int kMaxGridZ = 65535;
+constexpr int kMaxGridX = 1 << 30;
 
 pkv_status check_kv(const pkv_paged_kv* kv, const char* fn, KvView* view) {
   const std::string f(fn);
@@ -213,6 +214,21 @@ pkv_status pkv_gather_kv(const pkv_paged_kv* kv, const int32_t* block_tables,
                                    max_len, static_cast<uint16_t*>(k_out),
                                    static_cast<uint16_t*>(v_out),
                                    static_cast<hipStream_t>(stream)),
+                  fn);
+}
+
+pkv_status pkv_copy_blocks(const pkv_paged_kv* kv, const int32_t* pairs, int32_t num_pairs,
+                           void* stream) {
+  const char* fn = "pkv_copy_blocks";
+  KvView view;
+  pkv_status st = check_kv(kv, fn, &view);
+  if (st != PKV_OK) return st;
+  if (num_pairs < 0) return fail(PKV_ERR_INVALID_ARG, "pkv_copy_blocks: negative size");
+  if (num_pairs == 0) return ok();
+  if (pairs == nullptr) return fail(PKV_ERR_INVALID_ARG, "pkv_copy_blocks: NULL pointer");
+  if (num_pairs > kMaxGridX)
+    return fail(PKV_ERR_INVALID_ARG, "pkv_copy_blocks: too many pairs per call");
+  return launched(launch_copy_blocks(view, pairs, num_pairs, static_cast<hipStream_t>(stream)),
                   fn);
 }
 

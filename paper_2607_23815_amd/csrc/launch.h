@@ -26,6 +26,9 @@ hipError_t launch_gather_kv(const KvView& kv, const int32_t* block_tables, int32
                             int32_t max_len, uint16_t* k_out, uint16_t* v_out,
                             hipStream_t stream);
 
+hipError_t launch_copy_blocks(const KvView& kv, const int32_t* pairs, int32_t num_pairs,
+                              hipStream_t stream);
+
 hipError_t launch_prefill(const KvView& kv, const uint16_t* q, int32_t hq,
                           const int32_t* block_tables, int32_t max_blocks,
                           const int32_t* cached_lens, const int32_t* cu_new_lens,

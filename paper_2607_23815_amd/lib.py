@@ -34,12 +34,24 @@ PKV_ERR_SHARED_BLOCK_WRITE = 3
 PKV_ERR_UNSUPPORTED_SHAPE = 4
 PKV_ERR_NOT_FOUND = 5
 PKV_ERR_HIP = 6
+PKV_ERR_KEY_EXISTS = 7
+PKV_EVICT_LRU, PKV_EVICT_MRU = 0, 1
+PKV_PIN_EXPLICIT, PKV_PIN_VIRTUAL = 0, 1
 
 
 class PagedKV(ctypes.Structure):
     _fields_ = [("k_cache", c_void_p), ("v_cache", c_void_p), ("num_blocks", c_int32),
                 ("block_size", c_int32), ("num_kv_heads", c_int32), ("head_dim", c_int32)]
 
+
+class PoolStats(ctypes.Structure):
+    _fields_ = [("num_free", c_int32), ("num_entries", c_int32), ("cached_blocks", c_int32),
+                ("pinned_entries", c_int32), ("eviction", c_int32), ("pinning", c_int32),
+                ("hits", c_int64), ("misses", c_int64), ("evictions", c_int64),
+                ("cow_copies", c_int64)]
+
+
+c_uint64 = ctypes.c_uint64
 
 _SIGS = {
     "pkv_last_error": (ctypes.c_char_p, []),
@@ -54,6 +66,17 @@ _SIGS = {
     "pkv_seq_free": (c_int32, [c_void_p, c_int64]),
     "pkv_seq_len": (c_int32, [c_void_p, c_int64, P_int32]),
     "pkv_fill_block_tables": (c_int32, [c_void_p, P_int64, c_int32, c_int32, P_int32, P_int32]),
+    "pkv_pool_set_eviction": (c_int32, [c_void_p, c_int32]),
+    "pkv_pool_set_pinning": (c_int32, [c_void_p, c_int32]),
+    "pkv_pool_check_deadlock": (c_int32, [c_void_p, c_int32, c_int32, P_int32]),
+    "pkv_prefix_publish": (c_int32, [c_void_p, c_int64, c_uint64, c_int32]),
+    "pkv_prefix_attach": (c_int32, [c_void_p, c_uint64, P_int64, P_int32]),
+    "pkv_prefix_pin": (c_int32, [c_void_p, c_uint64]),
+    "pkv_prefix_unpin": (c_int32, [c_void_p, c_uint64]),
+    "pkv_prefix_release": (c_int32, [c_void_p, c_uint64]),
+    "pkv_seq_reserve_cow": (c_int32, [c_void_p, c_int64, c_int32, P_int32, c_int32, P_int32]),
+    "pkv_pool_get_stats": (c_int32, [c_void_p, ctypes.POINTER(PoolStats)]),
+    "pkv_copy_blocks": (c_int32, [ctypes.POINTER(PagedKV), c_void_p, c_int32, c_void_p]),
     "pkv_kv_append": (c_int32, [ctypes.POINTER(PagedKV), c_void_p, c_void_p, c_void_p, c_int32,
                                 c_void_p, c_void_p, c_int32, c_int32, c_int32, c_void_p]),
     "pkv_prefill_attention": (c_int32, [ctypes.POINTER(PagedKV), c_void_p, c_int32, c_void_p,
@@ -147,6 +170,59 @@ class BlockPool:
         if st not in (PKV_OK, PKV_ERR_OUT_OF_BLOCKS, PKV_ERR_SHARED_BLOCK_WRITE):
             _check(st)
         return st
+
+    def reserve_cow(self, seq: int, n: int):
+        """(status, [(source, copy), ...]); OK and OUT_OF_BLOCKS are expected outcomes."""
+        s = self.seq_len(seq)  # raises on an unknown sequence
+        del s
+        room = max(1, -(-n // self.block_size) + 1)  # blocks a write of n tokens can touch
+        buf = (c_int32 * (2 * room))()
+        cnt = c_int32()
+        st = _lib.pkv_seq_reserve_cow(self._h, seq, n, buf, room, ctypes.byref(cnt))
+        if st not in (PKV_OK, PKV_ERR_OUT_OF_BLOCKS):
+            _check(st)
+        return st, [(buf[2 * k], buf[2 * k + 1]) for k in range(cnt.value)]
+
+    def publish(self, seq: int, key: int, tokens: int) -> int:
+        """Status: OK or KEY_EXISTS; raises on other errors."""
+        st = _lib.pkv_prefix_publish(self._h, seq, key, tokens)
+        if st not in (PKV_OK, PKV_ERR_KEY_EXISTS):
+            _check(st)
+        return st
+
+    def attach(self, key: int):
+        """(sequence id, tokens) on a hit, None on a miss."""
+        sid, tok = c_int64(), c_int32()
+        st = _lib.pkv_prefix_attach(self._h, key, ctypes.byref(sid), ctypes.byref(tok))
+        if st == PKV_ERR_NOT_FOUND:
+            return None
+        _check(st)
+        return sid.value, tok.value
+
+    def pin(self, key: int) -> None:
+        _check(_lib.pkv_prefix_pin(self._h, key))
+
+    def unpin(self, key: int) -> None:
+        _check(_lib.pkv_prefix_unpin(self._h, key))
+
+    def release(self, key: int) -> None:
+        _check(_lib.pkv_prefix_release(self._h, key))
+
+    def set_eviction(self, policy: int) -> None:
+        _check(_lib.pkv_pool_set_eviction(self._h, policy))
+
+    def set_pinning(self, mode: int) -> None:
+        _check(_lib.pkv_pool_set_pinning(self._h, mode))
+
+    def check_deadlock(self, waiting: int, running: int) -> bool:
+        rec = c_int32()
+        _check(_lib.pkv_pool_check_deadlock(self._h, waiting, running, ctypes.byref(rec)))
+        return bool(rec.value)
+
+    def stats(self) -> dict:
+        st = PoolStats()
+        _check(_lib.pkv_pool_get_stats(self._h, ctypes.byref(st)))
+        return {name: int(getattr(st, name)) for name, _ in PoolStats._fields_}
 
     def commit(self, seq: int, n: int) -> None:
         _check(_lib.pkv_seq_commit(self._h, seq, n))
@@ -266,6 +342,16 @@ def pkv_decode_attention(k_cache, v_cache, q, block_tables, seq_lens, max_seq_le
         _dev_ptr(seq_lens, "seq_lens", torch.int32), b, int(max_seq_len), float(scale),
         _dev_ptr(out, "out", torch.bfloat16), _dev_ptr(lse, "lse", torch.float32),
         _dev_ptr(workspace, "workspace"), ws_bytes, _stream(stream)))
+
+
+def pkv_copy_blocks(k_cache, v_cache, pairs, stream=None) -> None:
+    """pairs: int32 GPU tensor [n][2] of (source block, copy)."""
+    import torch
+    kv = paged_kv(k_cache, v_cache)
+    if pairs.dim() != 2 or pairs.shape[1] != 2:
+        raise ValueError("pairs must be [n][2]")
+    _check(_lib.pkv_copy_blocks(ctypes.byref(kv), _dev_ptr(pairs, "pairs", torch.int32),
+                                int(pairs.shape[0]), _stream(stream)))
 
 
 def pkv_gather_kv(k_cache, v_cache, block_tables, lens, cu_lens, max_len: int, k_out, v_out,

@@ -124,6 +124,130 @@ def test_pool_matches_model_operation_for_operation(lib, seed):
                 assert pool.seq_len(ids[s]) == m.seqs[s].length
 
 
+def _status(fn, *args):
+    try:
+        res = fn(*args)
+        return 0, res
+    except Exception as e:  # PkvError
+        return e.status, None
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_pool_lifecycle_matches_model_operation_for_operation(lib, seed):
+    """Prefix cache, LRU/MRU eviction, pins, deadlock recovery and copy-on-write: the C++
+    pool and the oracle's model agree on every status, every copy pair, every table and
+    every counter over random operation sequences."""
+    from oracle.block_pool import EXPLICIT
+    rnd = random.Random(100 + seed)
+    nb = rnd.choice([12, 24, 48])
+    order = rnd.sample(range(nb), nb) if seed % 2 else None
+    m = BlockPoolModel(nb, 16, free_order=order)
+    pool = lib.BlockPool(nb, 16, free_order=order)
+    if seed % 3 == 2:
+        m.set_eviction(1)
+        pool.set_eviction(lib.PKV_EVICT_MRU)
+    ids, live, keys = {}, [], list(range(12))
+    for step in range(700):
+        r = rnd.random()
+        if r < 0.1 or not live:
+            a, _ = _apply(("create",), m, pool, ids)
+            live.append(a)
+        elif r < 0.4:
+            s, n = rnd.choice(live), rnd.randint(0, 60)
+            if rnd.random() < 0.6:
+                st_m, cp_m = m.reserve(s, n, cow=True)
+                st_l, cp_l = pool.reserve_cow(ids[s], n)
+                assert (int(st_m), cp_m) == (st_l, cp_l), step
+            else:
+                assert int(m.reserve(s, n)) == pool.reserve(ids[s], n), step
+        elif r < 0.5:
+            s = rnd.choice(live)
+            res = _apply(("commit", s, rnd.randint(0, m.seqs[s].pending)), m, pool, ids)
+            assert res[0] == res[1]
+        elif r < 0.6:
+            s = rnd.choice(live)
+            k, t = rnd.choice(keys), rnd.randint(0, m.seqs[s].length + 1)
+            st_m = int(m.publish(s, k, t))
+            st_l, res = _status(pool.publish, ids[s], k, t)
+            assert st_m == (res if st_l == 0 else st_l), step
+        elif r < 0.67:
+            k = rnd.choice(keys)
+            st_m, a, t = m.attach(k)
+            got = pool.attach(k)
+            if st_m == Status.OK:
+                assert got is not None and got[1] == t
+                ids[a] = got[0]
+                live.append(a)
+            else:
+                assert got is None
+        elif r < 0.73:
+            k = rnd.choice(keys)
+            pin = rnd.random() < 0.6
+            st_m = int((m.pin if pin else m.unpin)(k))
+            st_l, _ = _status(pool.pin if pin else pool.unpin, k)
+            assert st_m == st_l, step
+        elif r < 0.75:
+            k = rnd.choice(keys)
+            assert int(m.release(k)) == _status(pool.release, k)[0]
+        elif r < 0.78:
+            w, run = rnd.randint(0, 2), rnd.randint(0, 1)
+            assert m.check_deadlock(w, run)[1] == int(pool.check_deadlock(w, run))
+            if rnd.random() < 0.5:
+                m.set_pinning(EXPLICIT)
+                pool.set_pinning(lib.PKV_PIN_EXPLICIT)
+        elif r < 0.82:
+            s = rnd.choice(live)
+            res = _apply(("fork", s, (m.seqs[s].length // 16) * 16), m, pool, ids)
+            assert res == (0, 0)
+            live.append(max(m.seqs))
+        else:
+            s = live.pop(rnd.randrange(len(live)))
+            _apply(("free", s), m, pool, ids)
+        assert pool.stats() == m.stats(), step
+        if live and step % 20 == 0:
+            mb = max(len(m.seqs[s].blocks) for s in live) + 1
+            _, rows, lens = m.block_tables(live, mb)
+            tables, tl = pool.block_tables([ids[s] for s in live], mb)
+            assert np.array_equal(tables, np.asarray(rows, np.int32))
+            assert np.array_equal(tl, np.asarray(lens, np.int32))
+
+
+def test_pool_lifecycle_refusals(lib):
+    pool = lib.BlockPool(4, 16)
+    a = pool.create()
+    assert pool.reserve(a, 20) == lib.PKV_OK
+    pool.commit(a, 20)
+    assert pool.publish(a, 7, 20) == lib.PKV_OK
+    assert pool.publish(a, 7, 16) == lib.PKV_ERR_KEY_EXISTS
+    assert "already" in lib.pkv_last_error()
+    with pytest.raises(lib.PkvError) as e:
+        pool.publish(a, 8, 21)
+    assert e.value.status == lib.PKV_ERR_INVALID_ARG
+    assert pool.reserve(a, 1) == lib.PKV_ERR_SHARED_BLOCK_WRITE
+    # too little room for the copy pairs: refused, nothing changes
+    buf = (ctypes.c_int32 * 2)()
+    cnt = ctypes.c_int32(-1)
+    st = lib._lib.pkv_seq_reserve_cow(pool._h, a, 1, buf, 0, ctypes.byref(cnt))
+    assert st == lib.PKV_ERR_INVALID_ARG and cnt.value == 0
+    assert lib._lib.pkv_seq_reserve_cow(pool._h, a, 1, None, 1, ctypes.byref(cnt)) == \
+        lib.PKV_ERR_INVALID_ARG
+    assert pool.num_free() == 2
+    assert pool.attach(99) is None
+    assert pool.stats()["misses"] == 1
+    with pytest.raises(lib.PkvError) as e:
+        pool.unpin(7)
+    assert e.value.status == lib.PKV_ERR_INVALID_ARG
+    with pytest.raises(lib.PkvError) as e:
+        pool.set_eviction(2)
+    with pytest.raises(lib.PkvError) as e:
+        pool.check_deadlock(-1, 0)
+    st, copies = pool.reserve_cow(a, 1)
+    assert st == lib.PKV_OK and len(copies) == 1 and copies[0][0] == 1
+    pool.free(a)
+    pool.release(7)
+    assert pool.num_free() == 4
+
+
 def test_pool_refusals_change_nothing(lib):
     pool = lib.BlockPool(4, 16)
     a = pool.create()
