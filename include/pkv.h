@@ -95,7 +95,7 @@ pkv_status pkv_seq_create(pkv_pool* pool, int64_t* seq_id);
 pkv_status pkv_seq_fork(pkv_pool* pool, int64_t parent, int32_t shared_tokens, int64_t* child);
 
 /* Reserve room for new_tokens more tokens after the sequence's committed and already
- * reserved tokens. When too few blocks are free, idle unpinned cached prefixes are evicted
+ * reserved tokens. When too few blocks are free, unpinned cached prefixes are evicted
  * first (see the prefix cache below). All-or-nothing: OUT_OF_BLOCKS when even eviction
  * cannot free enough blocks and SHARED_BLOCK_WRITE when the range would write into a block
  * held by another sequence or a cached prefix; in both cases nothing changes (no eviction
@@ -126,8 +126,9 @@ pkv_status pkv_seq_len(const pkv_pool* pool, int64_t seq, int32_t* len);
  * blocks, entries are dropped in policy order until enough are free, all-or-nothing like
  * the reservation itself. Policy (Section 3 weighs both): least recently used first
  * (default) or most recently used first, by a logical clock that each publish and each hit
- * advances. Only idle entries are candidates: no sequence holds any of their blocks. A block
- * returns to the back of the free list when its last holder (sequence or entry) lets go.
+ * advances. Dropping an entry releases its references only: a block returns to the back of
+ * the free list when its last holder (sequence or entry) lets go, so a running sequence
+ * keeps the blocks it shares.
  *
  * Pinning (Section 6): under explicit pinning (default) an entry whose pin count is positive
  * is never evicted until it is unpinned; under virtual pinning pins protect nothing and the
@@ -158,6 +159,11 @@ pkv_status pkv_prefix_publish(pkv_pool* pool, int64_t seq, uint64_t key, int32_t
  * length is the entry's token count (*tokens), and the entry becomes most recently used.
  * Miss: NOT_FOUND, and nothing changes but the miss count. */
 pkv_status pkv_prefix_attach(pkv_pool* pool, uint64_t key, int64_t* seq, int32_t* tokens);
+
+/* Tokens cached under key (0 when absent). A pure query: no hit or miss is counted and the
+ * entry's recency does not change (a scheduler sizes a task's reservation with it before
+ * deciding to admit the task). */
+pkv_status pkv_prefix_lookup(const pkv_pool* pool, uint64_t key, int32_t* tokens);
 
 /* Pin counts of an entry (NOT_FOUND for an unknown key; unpin of an unpinned entry is
  * INVALID_ARG). */

@@ -25,11 +25,12 @@ Semantics (each from the paper, with the readings this project takes):
     through copy-on-write.
   * Eviction: when a reservation finds too few free blocks, resident entries are dropped in
     policy order until enough blocks are free -- least recently used first by default, most
-    recently used first as the alternative Section 3 weighs. An entry is a candidate only if
-    it is idle (no sequence holds any of its blocks: dropping it could not free a block in
-    use) and not protected by a pin. Recency is a logical clock advanced by publish and by
-    each hit. Reading: ties cannot occur (every publish and hit gets its own tick); the order
-    is by last use alone. The eviction is all-or-nothing like the reservation it serves.
+    recently used first as the alternative Section 3 weighs. Every entry not protected by a
+    pin is a candidate; dropping it releases its references, and only blocks that no sequence
+    or other entry still holds return to the free list (a running sequence keeps what it
+    shares). Recency is a logical clock advanced by publish and by each hit. Reading: ties
+    cannot occur (every publish and hit gets its own tick); the order is by last use alone.
+    The eviction is all-or-nothing like the reservation it serves.
   * Pinning (Section 6): under explicit pinning an entry with a positive pin count is never
     evicted until it is unpinned; under virtual pinning pins protect nothing and eviction
     order alone (LRU by default) decides. Pin counts are kept in both modes.
@@ -161,13 +162,9 @@ class BlockPoolModel:
         return Status.OK, copies
 
     # -- prefix cache ---------------------------------------------------------------------
-    def _idle(self, entry):
-        return not any(b in s.blocks for s in self.seqs.values() for b in entry.blocks)
-
     def _candidates(self):
         """Entries that may be evicted, in eviction order."""
-        keys = [k for k, e in self.entries.items()
-                if (e.pins == 0 or self.pinning == VIRTUAL) and self._idle(e)]
+        keys = [k for k, e in self.entries.items() if e.pins == 0 or self.pinning == VIRTUAL]
         return sorted(keys, key=lambda k: self.entries[k].last_use,
                       reverse=(self.eviction == MRU))
 
@@ -215,6 +212,11 @@ class BlockPoolModel:
             self.refcount[b] += 1
         self.entries[key] = _Entry(list(blocks), tokens, self._tick())
         return Status.OK
+
+    def lookup(self, key):
+        """Tokens cached under key, or 0 when absent; changes nothing (no hit, no recency)."""
+        e = self.entries.get(key)
+        return 0 if e is None else e.tokens
 
     def attach(self, key):
         """(status, sequence id, tokens): a hit makes a new sequence holding the entry."""

@@ -56,13 +56,10 @@ struct pkv_pool {
 
 namespace {
 
-// An entry may be evicted when no pin protects it and no sequence holds any of its blocks
-// (dropping it then cannot take a block from a running sequence).
+// An entry may be evicted when no pin protects it. Dropping it releases its references only:
+// blocks that a sequence or another entry still holds stay with them.
 bool evictable(const pkv_pool* pool, const pkv_pool::Entry& e) {
-  if (e.pins > 0 && pool->pinning == PKV_PIN_EXPLICIT) return false;
-  for (int32_t b : e.blocks)
-    if (pool->seq_refs[b] > 0) return false;
-  return true;
+  return e.pins == 0 || pool->pinning == PKV_PIN_VIRTUAL;
 }
 
 // Evictable entries in eviction order: by last use, oldest first (LRU) or newest first (MRU).
@@ -380,6 +377,14 @@ pkv_status pkv_prefix_attach(pkv_pool* pool, uint64_t key, int64_t* seq, int32_t
   pool->seqs.emplace(id, std::move(c));
   *seq = id;
   *tokens = e.tokens;
+  return ok();
+}
+
+pkv_status pkv_prefix_lookup(const pkv_pool* pool, uint64_t key, int32_t* tokens) {
+  if (pool == nullptr || tokens == nullptr)
+    return fail(PKV_ERR_INVALID_ARG, "pkv_prefix_lookup: NULL argument");
+  auto it = pool->entries.find(key);
+  *tokens = it == pool->entries.end() ? 0 : it->second.tokens;
   return ok();
 }
 

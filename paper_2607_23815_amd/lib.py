@@ -71,6 +71,7 @@ _SIGS = {
     "pkv_pool_check_deadlock": (c_int32, [c_void_p, c_int32, c_int32, P_int32]),
     "pkv_prefix_publish": (c_int32, [c_void_p, c_int64, c_uint64, c_int32]),
     "pkv_prefix_attach": (c_int32, [c_void_p, c_uint64, P_int64, P_int32]),
+    "pkv_prefix_lookup": (c_int32, [c_void_p, c_uint64, P_int32]),
     "pkv_prefix_pin": (c_int32, [c_void_p, c_uint64]),
     "pkv_prefix_unpin": (c_int32, [c_void_p, c_uint64]),
     "pkv_prefix_release": (c_int32, [c_void_p, c_uint64]),
@@ -198,6 +199,11 @@ class BlockPool:
             return None
         _check(st)
         return sid.value, tok.value
+
+    def lookup(self, key: int) -> int:
+        tok = c_int32()
+        _check(_lib.pkv_prefix_lookup(self._h, key, ctypes.byref(tok)))
+        return tok.value
 
     def pin(self, key: int) -> None:
         _check(_lib.pkv_prefix_pin(self._h, key))

@@ -172,6 +172,7 @@ def test_pool_lifecycle_matches_model_operation_for_operation(lib, seed):
             assert st_m == (res if st_l == 0 else st_l), step
         elif r < 0.67:
             k = rnd.choice(keys)
+            assert m.lookup(k) == pool.lookup(k)
             st_m, a, t = m.attach(k)
             got = pool.attach(k)
             if st_m == Status.OK:

@@ -167,21 +167,41 @@ def test_deadlock_recovery_unpins_everything_and_switches_to_virtual():
     check_invariants(m)
 
 
-def test_only_idle_entries_are_evicted():
+def test_eviction_keeps_blocks_a_running_sequence_shares():
     m = BlockPoolModel(4, BS)
     assert prefill_tuple(m, 1, 32) == Status.OK
     assert prefill_tuple(m, 2, 32) == Status.OK
-    st, user, _ = m.attach(1)  # entry 1 is in use, entry 2 is now the older one
+    st, user, _ = m.attach(1)  # entry 1 in use, and now the most recently used
     assert st == Status.OK
-    m.entries[1].last_use = 0  # make entry 1 the LRU candidate by recency
+    user_blocks = list(m.seqs[user].blocks)
     _, s = m.create()
-    assert m.reserve(s, 32) == Status.OK  # entry 2 goes: entry 1's blocks are in use
+    assert m.reserve(s, 32) == Status.OK  # LRU: entry 2 goes and frees its 2 blocks
     assert set(m.entries) == {1}
     before = state(m)
+    # dropping entry 1 would free nothing (user holds its blocks): refused, nothing evicted
     assert m.reserve(s, 1) == Status.OUT_OF_BLOCKS
     assert state(m) == before
     m.free_seq(user)
     assert m.reserve(s, 1) == Status.OK and m.entries == {}
+    check_invariants(m)
+
+
+def test_mru_eviction_may_drop_an_entry_in_use_without_taking_its_blocks():
+    m = BlockPoolModel(6, BS)
+    m.set_eviction(MRU)
+    assert prefill_tuple(m, 1, 32) == Status.OK
+    assert prefill_tuple(m, 2, 32) == Status.OK
+    _, user, _ = m.attach(2)  # entry 2 becomes the most recently used
+    user_blocks = list(m.seqs[user].blocks)
+    _, s = m.create()
+    assert m.reserve(s, 32) == Status.OK  # the 2 free blocks suffice: nothing evicted
+    assert len(m.entries) == 2
+    # one more block: MRU order drops entry 2 first (frees nothing: user holds it), then
+    # entry 1 (frees 2)
+    assert m.reserve(s, 1) == Status.OK
+    assert m.entries == {} and m.evictions == 2
+    assert m.seqs[user].blocks == user_blocks
+    assert all(m.refcount[b] == 1 for b in user_blocks)
     check_invariants(m)
 
 
