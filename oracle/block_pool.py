@@ -145,6 +145,9 @@ class BlockPoolModel:
         need = -(-end // self.block_size) - len(s.blocks) + len(shared)
         if not self._make_room(need):
             return Status.OUT_OF_BLOCKS, []
+        # an eviction above may have dropped a block's other holders: such a block is now
+        # private and is written in place
+        shared = [k for k in shared if self.refcount[s.blocks[k]] > 1]
         copies = []
         for k in shared:  # copies first, in table order
             old = s.blocks[k]

@@ -371,3 +371,30 @@ def test_oracle_block_copy_moves_whole_blocks_only():
     # a copy into a block that is itself a source reads the original source contents
     ck2, _ = oracle.copy_blocks(pk, pv, [(0, 1), (1, 2)])
     assert np.array_equal(ck2[2], pk[1]) and np.array_equal(ck2[1], pk[0])
+
+
+def test_eviction_inside_a_copy_on_write_reservation_makes_the_block_private():
+    """Regression: the shared partial block's only other holder is a cached entry that the
+    reservation itself evicts to make room. The block is then private: it is written in place,
+    not copied, and no block is lost."""
+    m = BlockPoolModel(5, BS)
+    _, s = m.create()
+    m.reserve(s, 24)
+    m.commit(s, 24)
+    assert m.publish(s, "p", 24) == Status.OK  # 2 blocks, the second half full
+    _, c, _ = m.attach("p")  # c shares both
+    m.free_seq(s)
+    _, s2 = m.create()
+    m.reserve(s2, 16)
+    m.commit(s2, 16)
+    assert m.publish(s2, "q", 16) == Status.OK  # 1 block
+    m.free_seq(s2)
+    _, other = m.create()
+    m.reserve(other, 16)  # 1 free block left
+    # growing c by 20 tokens: 1 copy + 1 growth block = 2 > 1 free. LRU order: "p" (frees
+    # nothing, c holds its blocks), then "q" (frees 1): enough. With "p" gone c holds its
+    # partial block alone.
+    st, copies = m.reserve(c, 20, cow=True)
+    assert st == Status.OK and m.entries == {} and copies == []
+    assert m.num_free() == 1
+    check_invariants(m)
