@@ -179,7 +179,8 @@ pkv_status pkv_prefix_release(pkv_pool* pool, uint64_t key);
  * (source block, copy) go to copies[2k], copies[2k+1] (host, room for max_copies pairs),
  * *num_copies receives their number; before appending, the caller copies those blocks'
  * contents on the device (pkv_copy_blocks). INVALID_ARG if more than max_copies copies are
- * needed; on any refusal nothing changes and *num_copies is 0. */
+ * needed; on any refusal nothing changes and *num_copies is 0. A block whose other holders
+ * are all evicted by this very reservation is private by then and is not copied. */
 pkv_status pkv_seq_reserve_cow(pkv_pool* pool, int64_t seq, int32_t new_tokens, int32_t* copies,
                                int32_t max_copies, int32_t* num_copies);
 
@@ -288,6 +289,116 @@ pkv_status pkv_gather_kv(const pkv_paged_kv* kv, const int32_t* block_tables,
                          int32_t max_blocks, const int32_t* lens, const int32_t* cu_lens,
                          int32_t num_seqs, int32_t max_len, void* k_out, void* v_out,
                          void* stream);
+
+/* ---------------------------------------------------------------------------------------
+ * Pipeline scheduler (Section 5, Algorithm 1; Section 6, memory management).
+ *
+ * A semantic query pipeline of num_stages stages: stage s runs one operator per task; a
+ * surviving task of a non-final stage is joined (Cartesian product) with fanout[s] right-side
+ * rows, creating dependent tasks that reuse its cached KV as their prefix; a final-stage task's
+ * result is output; a task whose predicate drops its tuple ends its branch. Tasks of stage 0
+ * are the num_tuples input tuples; task t of stage s+1 is row t % fanout[s] joined with task
+ * t / fanout[s] of stage s. Per task (all stages concatenated in stage order, stage s holding
+ * count_s = num_tuples * fanout[0] * ... * fanout[s-1] entries; fanout[num_stages-1] is
+ * ignored): suffix (tokens the task appends to its parent's prefix), out_len (tokens its
+ * request generates, 1..max_out) and filtered (non-zero: the predicate drops the tuple). These
+ * are the inputs that fix every outcome, so a run is deterministic.
+ *
+ * The scheduler follows Algorithm 1: per iteration, Launch admits waiting tasks stage by stage
+ * while the memory manager admits them; the engine advances the first max_batch admitted tasks
+ * by one step (a task's first step prefills its prompt and yields one token, each later step
+ * appends the previous token's KV and yields the next); Complete handles the finished ones
+ * (a task that reaches its token bound before its output is complete is interrupted, its bound
+ * doubled (at most max_out) and re-enqueued; children are enqueued and tracked; a parent's
+ * memory is released once all its children are); Rebalance moves budget: a saturated middle
+ * stage gives delta blocks to the last stage (from its own unused budget, else from the first
+ * stage with delta unused), and, from the last stage down, a starving stage gives delta to the
+ * stage before it (saturated: waiting > alpha * budget / minBudget; starving: waiting < beta *
+ * budget / minBudget). Token bounds: static per stage, or the nearest-rank 99th percentile of
+ * the output/input ratio of completed requests times the task's input length, once min_obs
+ * requests have completed (initial_bound before that). Memory is counted in 16-token blocks of
+ * a pool of num_blocks blocks that the run creates; completed prefixes are published in its
+ * prefix cache and, under explicit pinning, pinned until their children are released.
+ *
+ * Policies: ADAPTIVE is Algorithm 1; DEPTH_FIRST keeps its initial budgets (minBudget for all
+ * stages but the last, which takes the rest) and never rebalances; BREADTH_FIRST gives the
+ * first stage breadth_share of the pool statically; SEQUENTIAL runs one task at a time, the
+ * deepest ready stage first; BLOCKING runs each stage to completion before the next and leaves
+ * prefixes to the cache's eviction order (the materialising execution of Section 3).
+ * --------------------------------------------------------------------------------------- */
+#define PKV_MAX_STAGES 8
+enum { PKV_SCHED_ADAPTIVE = 0, PKV_SCHED_DEPTH_FIRST = 1, PKV_SCHED_BREADTH_FIRST = 2,
+       PKV_SCHED_SEQUENTIAL = 3, PKV_SCHED_BLOCKING = 4 };
+/* trace events: int32 quintuples (step, kind, stage, task, value) */
+enum {
+  PKV_EV_LAUNCH = 1,   /* value = 2 * charged blocks + 1 if the prefix is reused */
+  PKV_EV_DONE = 2,     /* completed and passed on; value = output tokens */
+  PKV_EV_FILTERED = 3, /* completed, dropped by its predicate; value = output tokens */
+  PKV_EV_OUTPUT = 4,   /* final-stage result; value = output tokens */
+  PKV_EV_RETRY = 5,    /* interrupted at its bound; value = the new bound */
+  PKV_EV_RELEASE = 6,  /* memory charge released; value = blocks */
+  PKV_EV_TRANSFER = 7  /* budget moved: stage = from, task = to, value = blocks */
+};
+
+typedef struct {
+  int32_t policy;        /* PKV_SCHED_* */
+  int32_t num_blocks;    /* KV blocks the pipeline may use */
+  int32_t max_out;       /* largest output of any request; bounds never exceed it */
+  int32_t delta;         /* budget transfer unit in blocks; 0 = the largest minBudget */
+  double alpha, beta;    /* queue thresholds */
+  double breadth_share;  /* BREADTH_FIRST: the first stage's share of num_blocks */
+  int32_t pinning;       /* PKV_PIN_* */
+  int32_t eviction;      /* PKV_EVICT_* */
+  int32_t min_obs;       /* completed requests before the percentile estimate is used */
+  int32_t max_batch;     /* tasks the engine advances per step */
+  int64_t max_steps;     /* the run fails (INVALID_ARG) if it has not finished by then */
+  int32_t static_bound[PKV_MAX_STAGES];   /* > 0: the stage's static token bound */
+  int32_t initial_bound[PKV_MAX_STAGES];  /* > 0: bound before min_obs observations
+                                             (0: max_out) */
+} pkv_sched_config;
+
+/* Device mode: each engine step also runs its attention work on the GPU through this
+ * library's calls (block copies for copy-on-write, KV append, prefill attention for tasks in
+ * their first step, decode attention for the others), on `stream`, timed with HIP events. The
+ * step's K/V rows and queries are read from rows 0.. of the caller's synthetic sources
+ * (bf16 [src_rows][num_kv_heads][head_dim] and [src_rows][num_q_heads][head_dim]; src_rows
+ * >= max_batch and >= every prompt). kv is a pool of at least num_blocks blocks; its contents
+ * are overwritten. The run allocates its own metadata, output and workspace buffers and frees
+ * them before returning. */
+typedef struct {
+  pkv_paged_kv kv;
+  int32_t num_q_heads;
+  const void* q_src;
+  const void* k_src;
+  const void* v_src;
+  int32_t src_rows;
+  void* stream;
+} pkv_sched_device;
+
+typedef struct {
+  int64_t steps, launches, retries, hits, misses;
+  int64_t prefill_tokens;  /* tokens prefilled (prompts, and recomputed prefixes on misses) */
+  int64_t reused_tokens;   /* prefix tokens taken from the cache instead */
+  int64_t decode_tokens;
+  int64_t cow_copies, evictions, outputs;
+  int32_t max_batch;       /* largest batch the engine ran */
+  double gpu_ms;           /* device mode: GPU time of all steps (events); 0 otherwise */
+  double wall_ms;          /* host wall time of the run */
+} pkv_sched_stats;
+
+/* Run the pipeline to completion (see above). num_tasks: the length of suffix, out_len and
+ * filtered, which must equal the sum of count_s (INVALID_ARG otherwise). dev NULL: scheduling
+ * only. trace (may be NULL
+ * when max_events is 0): room for max_events events; *num_events receives the number of
+ * events the run produced (those beyond max_events are counted, not written).
+ * final_budgets (may be NULL): int64 [num_stages]. INVALID_ARG for a bad configuration, a
+ * pool smaller than the stages' minimum budgets, or a run that cannot progress. */
+pkv_status pkv_sched_run(const pkv_sched_config* cfg, int32_t num_stages, int32_t num_tuples,
+                         const int32_t* fanout, int64_t num_tasks, const int32_t* suffix,
+                         const int32_t* out_len, const uint8_t* filtered,
+                         const pkv_sched_device* dev, int32_t* trace,
+                         int64_t max_events, int64_t* num_events, int64_t* final_budgets,
+                         pkv_sched_stats* stats);
 
 #ifdef __cplusplus
 }

@@ -146,6 +146,11 @@ pkv_status reserve_impl(pkv_pool* pool, int64_t seq, int32_t new_tokens, bool co
                                                 " blocks needed, " +
                                                 std::to_string(pool->free_list.size()) +
                                                 " free after eviction");
+  // an eviction above may have dropped a block's other holders: such a block is now private
+  // and is written in place
+  shared.erase(std::remove_if(shared.begin(), shared.end(),
+                              [&](size_t k) { return pool->refcount[s.blocks[k]] <= 1; }),
+               shared.end());
   for (size_t c = 0; c < shared.size(); ++c) {
     const int32_t old = s.blocks[shared[c]];
     const int32_t fresh = take_block(pool);

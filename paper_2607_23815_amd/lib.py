@@ -52,6 +52,34 @@ class PoolStats(ctypes.Structure):
 
 
 c_uint64 = ctypes.c_uint64
+c_double = ctypes.c_double
+
+PKV_MAX_STAGES = 8
+(PKV_SCHED_ADAPTIVE, PKV_SCHED_DEPTH_FIRST, PKV_SCHED_BREADTH_FIRST, PKV_SCHED_SEQUENTIAL,
+ PKV_SCHED_BLOCKING) = range(5)
+
+
+class SchedConfig(ctypes.Structure):
+    _fields_ = [("policy", c_int32), ("num_blocks", c_int32), ("max_out", c_int32),
+                ("delta", c_int32), ("alpha", c_double), ("beta", c_double),
+                ("breadth_share", c_double), ("pinning", c_int32), ("eviction", c_int32),
+                ("min_obs", c_int32), ("max_batch", c_int32), ("max_steps", c_int64),
+                ("static_bound", c_int32 * PKV_MAX_STAGES),
+                ("initial_bound", c_int32 * PKV_MAX_STAGES)]
+
+
+class SchedStats(ctypes.Structure):
+    _fields_ = [("steps", c_int64), ("launches", c_int64), ("retries", c_int64),
+                ("hits", c_int64), ("misses", c_int64), ("prefill_tokens", c_int64),
+                ("reused_tokens", c_int64), ("decode_tokens", c_int64),
+                ("cow_copies", c_int64), ("evictions", c_int64), ("outputs", c_int64),
+                ("max_batch", c_int32), ("gpu_ms", c_double), ("wall_ms", c_double)]
+
+class SchedDevice(ctypes.Structure):
+    _fields_ = [("kv", PagedKV), ("num_q_heads", c_int32), ("q_src", c_void_p),
+                ("k_src", c_void_p), ("v_src", c_void_p), ("src_rows", c_int32),
+                ("stream", c_void_p)]
+
 
 _SIGS = {
     "pkv_last_error": (ctypes.c_char_p, []),
@@ -78,6 +106,10 @@ _SIGS = {
     "pkv_seq_reserve_cow": (c_int32, [c_void_p, c_int64, c_int32, P_int32, c_int32, P_int32]),
     "pkv_pool_get_stats": (c_int32, [c_void_p, ctypes.POINTER(PoolStats)]),
     "pkv_copy_blocks": (c_int32, [ctypes.POINTER(PagedKV), c_void_p, c_int32, c_void_p]),
+    "pkv_sched_run": (c_int32, [ctypes.POINTER(SchedConfig), c_int32, c_int32, P_int32,
+                                c_int64, P_int32, P_int32, ctypes.POINTER(ctypes.c_uint8),
+                                ctypes.POINTER(SchedDevice), P_int32, c_int64, P_int64,
+                                P_int64, ctypes.POINTER(SchedStats)]),
     "pkv_kv_append": (c_int32, [ctypes.POINTER(PagedKV), c_void_p, c_void_p, c_void_p, c_int32,
                                 c_void_p, c_void_p, c_int32, c_int32, c_int32, c_void_p]),
     "pkv_prefill_attention": (c_int32, [ctypes.POINTER(PagedKV), c_void_p, c_int32, c_void_p,
@@ -251,6 +283,72 @@ class BlockPool:
                                           tables.ctypes.data_as(P_int32),
                                           lens.ctypes.data_as(P_int32)))
         return tables, lens
+
+
+# ----------------------------------------------------------------------------------------
+# Pipeline scheduler
+# ----------------------------------------------------------------------------------------
+def sched_config(policy, num_blocks, max_out, alpha=1.0, beta=0.5, delta=0, pinning=0,
+                 eviction=0, breadth_share=0.5, static_bound=None, initial_bound=None,
+                 min_obs=8, max_batch=256, max_steps=1_000_000) -> SchedConfig:
+    c = SchedConfig()
+    c.policy, c.num_blocks, c.max_out, c.delta = policy, num_blocks, max_out, delta
+    c.alpha, c.beta, c.breadth_share = alpha, beta, breadth_share
+    c.pinning, c.eviction, c.min_obs, c.max_batch = pinning, eviction, min_obs, max_batch
+    c.max_steps = max_steps
+    for s, v in enumerate(static_bound or []):
+        c.static_bound[s] = int(v)
+    for s, v in enumerate(initial_bound or []):
+        c.initial_bound[s] = int(v)
+    return c
+
+
+def pkv_sched_run(cfg: SchedConfig, fanout, suffix, out_len, filtered, device=None,
+                  max_events: int = 0):
+    """Run a pipeline (per-stage arrays, as the oracle's Pipeline takes them).
+    Returns (stats dict, trace int32 [n][5] (None when max_events is 0), final budgets).
+    device: None, or a dict(k_cache, v_cache, q_src, k_src, v_src[, stream]) of GPU tensors
+    for device mode."""
+    S = len(suffix)
+    fan = np.ascontiguousarray(np.asarray(list(fanout) + [1] * (S - len(fanout)),
+                                          dtype=np.int32)[:S])
+    suf = np.ascontiguousarray(np.concatenate([np.asarray(a) for a in suffix]).astype(np.int32))
+    out = np.ascontiguousarray(np.concatenate([np.asarray(a) for a in out_len]).astype(np.int32))
+    flt = np.ascontiguousarray(np.concatenate([np.asarray(a) for a in filtered]).astype(np.uint8))
+    trace = np.zeros((max(max_events, 1), 5), dtype=np.int32)
+    n_ev = c_int64()
+    budgets = np.zeros(S, dtype=np.int64)
+    stats = SchedStats()
+    dev_arg = None
+    if device is not None:
+        import torch
+        hq, d = int(device["q_src"].shape[1]), int(device["q_src"].shape[2])
+        kv = paged_kv(device["k_cache"], device["v_cache"])
+        dv = SchedDevice()
+        dv.kv = kv
+        dv.num_q_heads = hq
+        dv.q_src = _dev_ptr(device["q_src"], "q_src", torch.bfloat16)
+        dv.k_src = _dev_ptr(device["k_src"], "k_src", torch.bfloat16)
+        dv.v_src = _dev_ptr(device["v_src"], "v_src", torch.bfloat16)
+        dv.src_rows = int(min(device["q_src"].shape[0], device["k_src"].shape[0]))
+        dv.stream = _stream(device.get("stream"))
+        if int(device["k_src"].shape[2]) != d:
+            raise ValueError("q_src / k_src head dims differ")
+        dev_arg = ctypes.byref(dv)
+    if not (len(out) == len(suf) == len(flt)):
+        raise ValueError("suffix, out_len and filtered must have the same lengths")
+    _check(_lib.pkv_sched_run(ctypes.byref(cfg), S, int(len(suffix[0])),
+                              fan.ctypes.data_as(P_int32), int(len(suf)),
+                              suf.ctypes.data_as(P_int32),
+                              out.ctypes.data_as(P_int32),
+                              flt.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)), dev_arg,
+                              trace.ctypes.data_as(P_int32) if max_events else None,
+                              max_events, ctypes.byref(n_ev),
+                              budgets.ctypes.data_as(P_int64), ctypes.byref(stats)))
+    st = {name: getattr(stats, name) for name, _ in SchedStats._fields_}
+    tr = trace[: min(n_ev.value, max_events)] if max_events else None
+    st["num_events"] = n_ev.value
+    return st, tr, budgets
 
 
 # ----------------------------------------------------------------------------------------
