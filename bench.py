@@ -493,6 +493,62 @@ def reuse_vs_recompute(args, lib, torch):
     return out
 
 
+def pipelines(args, lib, torch):
+    """Section 5's scheduler driving the attention path: the synthetic pipelines (filter then
+    map, a map then a 17-way Cartesian product, three stages) run to completion under each
+    policy, every engine step's append, block copies and prefill/decode attention on the GPU
+    (one attention layer, Llama-3-8B heads). The KV pool holds about 64 first-stage tuples'
+    prefixes, so the table does not fit: blocking execution loses its prefixes to the cache
+    (Section 3's cliff) while the memory-aware schedule keeps them. gpu_ms is the summed GPU
+    time of the steps; the host schedules between steps (wall_ms)."""
+    from workloads.pipelines import PIPELINES, make_pipeline
+    hq, hkv, d, src_rows = 32, 8, 128, 8192
+    g = torch.Generator(device="cuda")
+    g.manual_seed(7)
+
+    def rnd(*shape):
+        return torch.randn(*shape, generator=g, device="cuda").to(torch.bfloat16)
+    q_src, k_src, v_src = rnd(src_rows, hq, d), rnd(src_rows, hkv, d), rnd(src_rows, hkv, d)
+    names = {0: "adaptive_virtual", 1: "depth_first", 2: "breadth_first", 3: "sequential",
+             4: "blocking"}
+    out = {}
+    for spec in PIPELINES:
+        pd = make_pipeline(spec)
+        S = len(pd["suffix"])
+        mean0 = float(np.mean(pd["suffix"][0]) + np.mean(pd["out_len"][0]))
+        nb = int(64 * math.ceil(mean0 / 16)) + 2048
+        predicate = [bool(np.max(pd["out_len"][s]) <= 3) for s in range(S)]
+        kw = dict(max_out=64, max_batch=64, static_bound=[8 if p else 0 for p in predicate],
+                  initial_bound=[16] * S, pinning=lib.PKV_PIN_VIRTUAL)
+        pool_k = torch.zeros((nb, hkv, d // 8, 16, 8), dtype=torch.bfloat16, device="cuda")
+        pool_v = torch.zeros((nb, hkv, d, 16), dtype=torch.bfloat16, device="cuda")
+        dev = dict(k_cache=pool_k, v_cache=pool_v, q_src=q_src, k_src=k_src, v_src=v_src)
+        runs = {}
+        plist = [(0, lib.PKV_PIN_VIRTUAL), (0, lib.PKV_PIN_EXPLICIT), (1, None), (2, None),
+                 (4, None)]
+        if spec.num_tuples <= 400:
+            plist.append((3, None))
+        for policy, pin in plist:
+            name = names[policy] if policy != 0 or pin == lib.PKV_PIN_VIRTUAL else \
+                "adaptive_explicit"
+            cfg = lib.sched_config(policy, nb, **{**kw, **({"pinning": pin} if pin is not None
+                                                           else {})})
+            st, _, bud = lib.pkv_sched_run(cfg, pd["fanout"], pd["suffix"], pd["out_len"],
+                                           pd["filtered"], device=dev)
+            runs[name] = {k: (round(v, 3) if isinstance(v, float) else int(v))
+                          for k, v in st.items()}
+            runs[name]["input_tuples_per_s_gpu"] = spec.num_tuples / (st["gpu_ms"] / 1e3)
+            log(f"[bench]   {spec.name} {name}: gpu {st['gpu_ms']:.1f} ms, steps "
+                f"{st['steps']}, hits {st['hits']}, misses {st['misses']}")
+        base = runs["blocking"]["gpu_ms"]
+        for r in runs.values():
+            r["speedup_vs_blocking"] = base / r["gpu_ms"]
+        out[spec.name] = {"num_tuples": spec.num_tuples, "num_blocks": nb, "runs": runs}
+        del pool_k, pool_v, dev
+        torch.cuda.empty_cache()
+    return out
+
+
 def profile_copy(args, torch):
     """A plain device copy of known size (1 GiB read + 1 GiB written per launch): the
     reference that scales the L2<->HBM byte counters to bytes."""
@@ -586,6 +642,8 @@ def main():
         log("[bench] secondary workloads ...")
         res["secondary"] = secondary(args, lib, torch)
         res["secondary"]["reuse_vs_recompute"] = reuse_vs_recompute(args, lib, torch)
+        log("[bench] pipelines under the scheduler ...")
+        res["secondary"]["pipelines"] = pipelines(args, lib, torch)
         log("[bench] secondary done")
     print(json.dumps(res), flush=True)
 

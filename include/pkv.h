@@ -362,7 +362,8 @@ typedef struct {
  * their first step, decode attention for the others), on `stream`, timed with HIP events. The
  * step's K/V rows and queries are read from rows 0.. of the caller's synthetic sources
  * (bf16 [src_rows][num_kv_heads][head_dim] and [src_rows][num_q_heads][head_dim]; src_rows
- * >= max_batch and >= every prompt). kv is a pool of at least num_blocks blocks; its contents
+ * >= max_batch and >= the longest prefix plus suffix of any task, checked before anything
+ * runs). kv is a pool of at least num_blocks blocks; its contents
  * are overwritten. The run allocates its own metadata, output and workspace buffers and frees
  * them before returning. */
 typedef struct {

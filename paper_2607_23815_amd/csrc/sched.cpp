@@ -84,10 +84,18 @@ class DeviceRunner {
     const size_t meta_ints = (size_t)max_batch * max_table + 4 * (size_t)max_batch + 8 +
                              2 * (size_t)max_batch;
     meta_bytes_ = meta_ints * sizeof(int32_t);
+    // The decode workspace depends on the batch and the longest sequence, and not
+    // monotonically in the latter (shorter sequences may split into more pieces). Size it for
+    // the most pieces any call can have: sequences of up to max_kv_len keys cut into splits of
+    // at least 64 keys, on top of the space the sequence order takes.
     size_t ws = 0;
-    for (int32_t n = 1; n <= max_batch; ++n)
-      ws = std::max(ws, pkv_decode_workspace_bytes(n, dev_.num_q_heads, kv.num_kv_heads,
-                                                   kv.head_dim, (int32_t)max_kv_len));
+    for (int32_t n = 1; n <= max_batch; ++n) {
+      const size_t order = pkv_decode_workspace_bytes(n, dev_.num_q_heads, kv.num_kv_heads,
+                                                      kv.head_dim, 1);
+      const size_t parts = (size_t)n * dev_.num_q_heads * (size_t)((max_kv_len + 63) / 64) *
+                           (size_t)(kv.head_dim + 2) * sizeof(float);
+      ws = std::max(ws, order + parts);
+    }
     ws_bytes_ = ws;
     const size_t out_bytes = (size_t)dev_.src_rows * dev_.num_q_heads * kv.head_dim * 2;
     hipError_t e = hipMalloc(&meta_dev_, meta_bytes_);
@@ -204,6 +212,8 @@ class DeviceRunner {
   }
 
   void release() {
+    if (dev_.stream != nullptr || meta_dev_ != nullptr)
+      (void)hipStreamSynchronize(static_cast<hipStream_t>(dev_.stream));
     if (meta_dev_) (void)hipFree(meta_dev_);
     if (meta_host_) (void)hipHostFree(meta_host_);
     if (out_) (void)hipFree(out_);
@@ -292,6 +302,12 @@ class Sched {
   }
 
   ~Sched() { pkv_pool_destroy(pool_); }
+
+  int64_t max_prompt() const {
+    int64_t m = 0;
+    for (size_t k = 0; k < prefix_.size(); ++k) m = std::max(m, prefix_[k] + suffix_[k]);
+    return m;
+  }
 
   int64_t max_kv_len() const {
     int64_t m = 0;
@@ -686,6 +702,9 @@ pkv_status pkv_sched_run(const pkv_sched_config* cfg, int32_t num_stages, int32_
     if (dev->kv.num_blocks < cfg->num_blocks)
       return fail(PKV_ERR_INVALID_ARG, "pkv_sched_run: the device pool has fewer blocks than "
                                        "num_blocks");
+    if (sched.max_prompt() > dev->src_rows)
+      return fail(PKV_ERR_INVALID_ARG, "pkv_sched_run: src_rows is smaller than the longest "
+                                       "prompt (prefix and suffix)");
     const int64_t max_len = sched.max_kv_len();
     if (max_len > INT32_MAX / 2) return fail(PKV_ERR_INVALID_ARG, "pkv_sched_run: too long");
     if ((st = runner.init(dev, cfg->max_batch, max_len, (int32_t)cdiv(max_len, kBS))) != PKV_OK)
