@@ -15,7 +15,8 @@ CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libpkv.so")
 ARCH = "gfx950"
 
-SOURCES = ["pool.cpp", "sched.cpp", "api.cpp", "kv_copy.hip", "decode.hip", "prefill.hip"]
+SOURCES = ["pool.cpp", "sched.cpp", "api.cpp", "kv_copy.hip", "block_copy.hip", "decode.hip",
+           "prefill.hip"]
 
 
 def hipcc() -> str:

@@ -1,5 +1,5 @@
-// KV append (scatter of new tokens' K/V into their sequences' pool slots), KV gather (the
-// reverse, for tests) and whole-block copies (copy-on-write), for gfx950.
+// KV append (scatter of new tokens' K/V into their sequences' pool slots) and KV gather (the
+// reverse, for tests), for gfx950.
 //
 // One workgroup moves one (sequence, 16-token block, kv head): at most 16 tokens x head_dim
 // for K and for V, i.e. one 4 KB K slab and one 4 KB V slab at head_dim 128.
@@ -124,33 +124,7 @@ __global__ __launch_bounds__(256) void gather_kv_kernel(
   }
 }
 
-// Copy-on-write block copy: workgroup (k, which) copies the K (which = 0) or V (which = 1)
-// region of block pairs[2k] to block pairs[2k+1]. A block's region for all heads is one
-// contiguous span of hkv * D * 16 elements in either cache, so this is a plain 16-byte
-// vector copy, coalesced across the workgroup.
-__global__ __launch_bounds__(256) void copy_blocks_kernel(uint16_t* __restrict__ k_cache,
-                                                          uint16_t* __restrict__ v_cache,
-                                                          const int32_t* __restrict__ pairs,
-                                                          int32_t num_blocks, int64_t span) {
-  const int32_t src = pairs[2 * blockIdx.x];
-  const int32_t dst = pairs[2 * blockIdx.x + 1];
-  if (src < 0 || src >= num_blocks || dst < 0 || dst >= num_blocks || src == dst) return;
-  uint16_t* base = blockIdx.y == 0 ? k_cache : v_cache;
-  const u32x4* from = reinterpret_cast<const u32x4*>(base + (size_t)src * span);
-  u32x4* to = reinterpret_cast<u32x4*>(base + (size_t)dst * span);
-  const int64_t n = span / 8;  // 16-byte chunks
-  for (int64_t c = threadIdx.x; c < n; c += 256) to[c] = from[c];
-}
-
 }  // namespace
-
-hipError_t launch_copy_blocks(const KvView& kv, const int32_t* pairs, int32_t num_pairs,
-                              hipStream_t stream) {
-  const int64_t span = (int64_t)kv.hkv * kv.head_dim * kBlockSize;
-  hipLaunchKernelGGL(copy_blocks_kernel, dim3(num_pairs, 2), dim3(256), 0, stream, kv.k, kv.v,
-                     pairs, kv.num_blocks, span);
-  return hipGetLastError();
-}
 
 hipError_t launch_kv_append(const KvView& kv, const uint16_t* k_new, const uint16_t* v_new,
                             const int32_t* block_tables, int32_t max_blocks,
