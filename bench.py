@@ -524,15 +524,19 @@ def pipelines(args, lib, torch):
         pool_v = torch.zeros((nb, hkv, d, 16), dtype=torch.bfloat16, device="cuda")
         dev = dict(k_cache=pool_k, v_cache=pool_v, q_src=q_src, k_src=k_src, v_src=v_src)
         runs = {}
-        plist = [(0, lib.PKV_PIN_VIRTUAL), (0, lib.PKV_PIN_EXPLICIT), (1, None), (2, None),
-                 (4, None)]
+        plist = [(0, lib.PKV_PIN_VIRTUAL, 0), (0, lib.PKV_PIN_EXPLICIT, 0),
+                 (0, lib.PKV_PIN_EXPLICIT, 4096), (1, None, 0), (2, None, 0), (4, None, 0)]
         if spec.num_tuples <= 400:
-            plist.append((3, None))
-        for policy, pin in plist:
+            plist.append((3, None, 0))
+        for policy, pin, budget in plist:
             name = names[policy] if policy != 0 or pin == lib.PKV_PIN_VIRTUAL else \
                 "adaptive_explicit"
-            cfg = lib.sched_config(policy, nb, **{**kw, **({"pinning": pin} if pin is not None
-                                                           else {})})
+            if budget:
+                name += f"_chunked_{budget}"
+            over = {"max_step_tokens": budget}
+            if pin is not None:
+                over["pinning"] = pin
+            cfg = lib.sched_config(policy, nb, **{**kw, **over})
             st, _, bud = lib.pkv_sched_run(cfg, pd["fanout"], pd["suffix"], pd["out_len"],
                                            pd["filtered"], device=dev)
             runs[name] = {k: (round(v, 3) if isinstance(v, float) else int(v))

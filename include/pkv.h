@@ -307,7 +307,8 @@ pkv_status pkv_gather_kv(const pkv_paged_kv* kv, const int32_t* block_tables,
  * The scheduler follows Algorithm 1: per iteration, Launch admits waiting tasks stage by stage
  * while the memory manager admits them; the engine advances the first max_batch admitted tasks
  * by one step (a task's first step prefills its prompt and yields one token, each later step
- * appends the previous token's KV and yields the next); Complete handles the finished ones
+ * appends the previous token's KV and yields the next; with max_step_tokens, prompts are
+ * prefilled in chunks that fit the step's token budget after the batch's decodes); Complete handles the finished ones
  * (a task that reaches its token bound before its output is complete is interrupted, its bound
  * doubled (at most max_out) and re-enqueued; children are enqueued and tracked; a parent's
  * memory is released once all its children are); Rebalance moves budget: a saturated middle
@@ -352,6 +353,9 @@ typedef struct {
   int32_t min_obs;       /* completed requests before the percentile estimate is used */
   int32_t max_batch;     /* tasks the engine advances per step */
   int64_t max_steps;     /* the run fails (INVALID_ARG) if it has not finished by then */
+  int32_t max_step_tokens; /* > 0: chunked prefill, at most this many tokens per step (the
+                              batch's decodes first, one each, then prompt chunks in queue
+                              order); 0: whole prompts */
   int32_t static_bound[PKV_MAX_STAGES];   /* > 0: the stage's static token bound */
   int32_t initial_bound[PKV_MAX_STAGES];  /* > 0: bound before min_obs observations
                                              (0: max_out) */
@@ -382,6 +386,7 @@ typedef struct {
   int64_t reused_tokens;   /* prefix tokens taken from the cache instead */
   int64_t decode_tokens;
   int64_t cow_copies, evictions, outputs;
+  int64_t prefill_chunks;  /* prompt pieces prefilled (one per prompt without a budget) */
   int32_t max_batch;       /* largest batch the engine ran */
   double gpu_ms;           /* device mode: GPU time of all steps (events); 0 otherwise */
   double wall_ms;          /* host wall time of the run */

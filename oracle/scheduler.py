@@ -38,7 +38,10 @@ Readings where the paper is silent (the library implements the same ones):
     task's first step prefills its prompt (suffix, or prefix + suffix on a miss) and yields one
     output token; each later step appends the previous token's KV and yields one more. A task
     with out_len output tokens takes out_len steps and leaves P + suffix + out_len - 1 tokens of
-    KV, the prefix its children reuse.
+    KV, the prefix its children reuse. With a per-step token budget (chunked prefill), the
+    decoding tasks of the batch go first, one token each, in queue order, and the rest of the
+    budget goes to prompt chunks, in queue order; a prompt yields its first token with its last
+    chunk (a chunk attends over the cached prefix and the earlier chunks).
   * The bound is fixed when the task is admitted; before min_obs observations an estimated stage
     uses its initial bound; the 99th percentile is the nearest-rank one (rank ceil(0.99 n));
     the ratio and its product with the input length are computed in double precision and
@@ -101,7 +104,8 @@ class Pipeline:
 class Config:
     def __init__(self, policy, num_blocks, max_out, alpha=1.0, beta=0.5, delta=0,
                  pinning=EXPLICIT, eviction=LRU, breadth_share=0.5, static_bound=None,
-                 initial_bound=None, min_obs=8, max_batch=256, max_steps=1_000_000):
+                 initial_bound=None, min_obs=8, max_batch=256, max_steps=1_000_000,
+                 max_step_tokens=0):
         self.policy = policy
         self.num_blocks = num_blocks
         self.max_out = max_out
@@ -111,6 +115,7 @@ class Config:
         self.static_bound = static_bound
         self.initial_bound = initial_bound
         self.min_obs, self.max_batch, self.max_steps = min_obs, max_batch, max_steps
+        self.max_step_tokens = max_step_tokens  # 0: no budget (whole prompts)
 
 
 class _Task:
@@ -122,7 +127,8 @@ class _Task:
         self.hit = True
         self.seq = 0
         self.cached = 0      # prefix tokens reused from the cache
-        self.prompt = 0      # tokens the first step prefills
+        self.prompt = 0      # prompt tokens to prefill
+        self.prefilled = 0   # of which done
         self.generated = 0
         self.children_left = 0
 
@@ -146,7 +152,8 @@ class SchedulerModel:
         self.trace, self.out = [], []
         self.step = 0
         self.stats = dict(steps=0, launches=0, retries=0, hits=0, misses=0, prefill_tokens=0,
-                          reused_tokens=0, decode_tokens=0, cow_copies=0, max_batch=0)
+                          reused_tokens=0, decode_tokens=0, cow_copies=0, max_batch=0,
+                          prefill_chunks=0)
 
     # -- memory manager ---------------------------------------------------------------------
     def _initial_budgets(self):
@@ -218,7 +225,7 @@ class SchedulerModel:
             t.cached, t.prompt = 0, P + suf
             self.stats["misses"] += 1
         self.used[self._charged_stage(t)] += charge
-        t.generated = 0
+        t.generated = t.prefilled = 0
         self.stats["launches"] += 1
         self.trace.append((self.step, EV_LAUNCH, s, i, 2 * charge + (1 if hit else 0)))
 
@@ -301,13 +308,36 @@ class SchedulerModel:
         as (task, kind) in queue order, kind 0 = completed, 1 = interrupted at its bound."""
         batch = self.running[: self.c.max_batch]
         self.stats["max_batch"] = max(self.stats["max_batch"], len(batch))
+        if self.c.max_step_tokens <= 0:
+            take = {id(t): (t.prompt - t.prefilled if t.generated == 0 else 1) for t in batch}
+        else:  # chunked prefill: decodes first, then prompt chunks, in queue order
+            left = self.c.max_step_tokens
+            take = {}
+            for t in batch:
+                if t.generated > 0 and left > 0:
+                    take[id(t)] = 1
+                    left -= 1
+            for t in batch:
+                if t.generated == 0:
+                    rest = t.prompt - t.prefilled
+                    if rest == 0 or left > 0:
+                        take[id(t)] = min(rest, left)
+                        left -= take[id(t)]
         done = []
         for t in batch:
+            if id(t) not in take:
+                continue
+            n = take[id(t)]
             s, i = t.stage, t.idx
             if t.generated == 0:
-                self.pool.commit(t.seq, t.prompt)
-                self.stats["prefill_tokens"] += t.prompt
-                self.stats["reused_tokens"] += t.cached
+                self.pool.commit(t.seq, n)
+                self.stats["prefill_tokens"] += n
+                if t.prefilled == 0:
+                    self.stats["reused_tokens"] += t.cached
+                self.stats["prefill_chunks"] += 1
+                t.prefilled += n
+                if t.prefilled < t.prompt:
+                    continue
             else:
                 self.pool.commit(t.seq, 1)
                 self.stats["decode_tokens"] += 1

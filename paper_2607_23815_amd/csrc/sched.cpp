@@ -55,7 +55,8 @@ struct Task {
   bool hit = true;
   int64_t seq = 0;
   int64_t cached = 0;  // prefix tokens reused from the cache
-  int64_t prompt = 0;  // tokens the first step prefills
+  int64_t prompt = 0;  // prompt tokens to prefill
+  int64_t prefilled = 0;  // of which done
   int32_t generated = 0;
   int32_t children_left = 0;
 };
@@ -475,6 +476,7 @@ class Sched {
     }
     used_[charged_stage(t)] += charge;
     t.generated = 0;
+    t.prefilled = 0;
     stats_.launches += 1;
     event(PKV_EV_LAUNCH, s, t.idx, 2 * charge + (hit ? 1 : 0));
     running_.push_back(ti);
@@ -520,15 +522,43 @@ class Sched {
   pkv_status engine_step(DeviceRunner* dev, std::vector<std::pair<int64_t, int>>* done) {
     const size_t nb = std::min(running_.size(), (size_t)c_.max_batch);
     stats_.max_batch = std::max(stats_.max_batch, (int32_t)nb);
+    // tokens each batch task takes this step (-1: not scheduled)
+    std::vector<int64_t> take(nb, -1);
+    if (c_.max_step_tokens <= 0) {
+      for (size_t k = 0; k < nb; ++k) {
+        const Task& t = tasks_[running_[k]];
+        take[k] = t.generated == 0 ? t.prompt - t.prefilled : 1;
+      }
+    } else {  // chunked prefill: decodes first, then prompt chunks, in queue order
+      int64_t left = c_.max_step_tokens;
+      for (size_t k = 0; k < nb; ++k)
+        if (tasks_[running_[k]].generated > 0 && left > 0) {
+          take[k] = 1;
+          left -= 1;
+        }
+      for (size_t k = 0; k < nb; ++k) {
+        const Task& t = tasks_[running_[k]];
+        if (t.generated != 0) continue;
+        const int64_t rest = t.prompt - t.prefilled;
+        if (rest == 0 || left > 0) {
+          take[k] = std::min(rest, left);
+          left -= take[k];
+        }
+      }
+    }
     std::vector<StepItem> pre, dec;
     for (size_t k = 0; k < nb; ++k) {
+      if (take[k] < 0) continue;
       Task& t = tasks_[running_[k]];
       pkv_status st;
       if (t.generated == 0) {
-        pre.push_back({t.seq, (int32_t)t.cached, (int32_t)t.prompt});
-        if ((st = pkv_seq_commit(pool_, t.seq, (int32_t)t.prompt)) != PKV_OK) return st;
-        stats_.prefill_tokens += t.prompt;
-        stats_.reused_tokens += t.cached;
+        pre.push_back({t.seq, (int32_t)(t.cached + t.prefilled), (int32_t)take[k]});
+        if ((st = pkv_seq_commit(pool_, t.seq, (int32_t)take[k])) != PKV_OK) return st;
+        stats_.prefill_tokens += take[k];
+        if (t.prefilled == 0) stats_.reused_tokens += t.cached;
+        stats_.prefill_chunks += 1;
+        t.prefilled += take[k];
+        if (t.prefilled < t.prompt) continue;
       } else {
         dec.push_back({t.seq, (int32_t)(t.cached + t.prompt + t.generated - 1), 1});
         if ((st = pkv_seq_commit(pool_, t.seq, 1)) != PKV_OK) return st;
@@ -689,7 +719,7 @@ pkv_status pkv_sched_run(const pkv_sched_config* cfg, int32_t num_stages, int32_
     return fail(PKV_ERR_INVALID_ARG, "pkv_sched_run: need 1..8 stages and at least one tuple");
   if (cfg->policy < PKV_SCHED_ADAPTIVE || cfg->policy > PKV_SCHED_BLOCKING ||
       cfg->num_blocks < 1 || cfg->max_out < 1 || cfg->max_batch < 1 || cfg->min_obs < 1 ||
-      cfg->delta < 0 || !(cfg->alpha > 0.0) || !(cfg->beta >= 0.0) ||
+      cfg->delta < 0 || cfg->max_step_tokens < 0 || !(cfg->alpha > 0.0) || !(cfg->beta >= 0.0) ||
       !(cfg->breadth_share >= 0.0 && cfg->breadth_share <= 1.0) ||
       (trace == nullptr && max_events > 0) || max_events < 0)
     return fail(PKV_ERR_INVALID_ARG, "pkv_sched_run: bad configuration");

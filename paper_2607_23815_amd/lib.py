@@ -64,6 +64,7 @@ class SchedConfig(ctypes.Structure):
                 ("delta", c_int32), ("alpha", c_double), ("beta", c_double),
                 ("breadth_share", c_double), ("pinning", c_int32), ("eviction", c_int32),
                 ("min_obs", c_int32), ("max_batch", c_int32), ("max_steps", c_int64),
+                ("max_step_tokens", c_int32),
                 ("static_bound", c_int32 * PKV_MAX_STAGES),
                 ("initial_bound", c_int32 * PKV_MAX_STAGES)]
 
@@ -73,7 +74,7 @@ class SchedStats(ctypes.Structure):
                 ("hits", c_int64), ("misses", c_int64), ("prefill_tokens", c_int64),
                 ("reused_tokens", c_int64), ("decode_tokens", c_int64),
                 ("cow_copies", c_int64), ("evictions", c_int64), ("outputs", c_int64),
-                ("max_batch", c_int32), ("gpu_ms", c_double), ("wall_ms", c_double)]
+                ("prefill_chunks", c_int64), ("max_batch", c_int32), ("gpu_ms", c_double), ("wall_ms", c_double)]
 
 class SchedDevice(ctypes.Structure):
     _fields_ = [("kv", PagedKV), ("num_q_heads", c_int32), ("q_src", c_void_p),
@@ -290,12 +291,14 @@ class BlockPool:
 # ----------------------------------------------------------------------------------------
 def sched_config(policy, num_blocks, max_out, alpha=1.0, beta=0.5, delta=0, pinning=0,
                  eviction=0, breadth_share=0.5, static_bound=None, initial_bound=None,
-                 min_obs=8, max_batch=256, max_steps=1_000_000) -> SchedConfig:
+                 min_obs=8, max_batch=256, max_steps=1_000_000,
+                 max_step_tokens=0) -> SchedConfig:
     c = SchedConfig()
     c.policy, c.num_blocks, c.max_out, c.delta = policy, num_blocks, max_out, delta
     c.alpha, c.beta, c.breadth_share = alpha, beta, breadth_share
     c.pinning, c.eviction, c.min_obs, c.max_batch = pinning, eviction, min_obs, max_batch
     c.max_steps = max_steps
+    c.max_step_tokens = max_step_tokens
     for s, v in enumerate(static_bound or []):
         c.static_bound[s] = int(v)
     for s, v in enumerate(initial_bound or []):

@@ -25,14 +25,16 @@ def _device(torch, num_blocks, hq=32, hkv=8, d=128, src_rows=8192, seed=0):
 
 
 @pytest.mark.parametrize("spec", PIPELINES, ids=lambda s: s.name)
-@pytest.mark.parametrize("policy", [0, 4])
-def test_device_mode_runs_the_same_schedule(gpu_lib, spec, policy):
+@pytest.mark.parametrize("policy,budget", [(0, 0), (4, 0), (0, 200)])
+def test_device_mode_runs_the_same_schedule(gpu_lib, spec, policy, budget):
+    """budget > 0: chunked prefill (prompt pieces attend over the cache and earlier pieces)."""
     import torch
     lib = gpu_lib
-    say(f"[sched device] {spec.name} policy {policy}")
+    say(f"[sched device] {spec.name} policy {policy} step budget {budget}")
     d = make_pipeline(spec.scaled(24))
     nb = 1500
-    kw = dict(max_out=64, initial_bound=[8] * len(d["suffix"]), max_batch=16, pinning=1)
+    kw = dict(max_out=64, initial_bound=[8] * len(d["suffix"]), max_batch=16, pinning=1,
+              max_step_tokens=budget)
     cfg = lib.sched_config(policy, nb, **kw)
     args = (d["fanout"], d["suffix"], d["out_len"], d["filtered"])
     st0, tr0, b0 = lib.pkv_sched_run(cfg, *args, max_events=200000)

@@ -11,7 +11,8 @@ from oracle.scheduler import Config, Pipeline, run_schedule
 from workloads.pipelines import PIPELINES, make_pipeline
 
 STAT_KEYS = ("steps", "launches", "retries", "hits", "misses", "prefill_tokens",
-             "reused_tokens", "decode_tokens", "cow_copies", "max_batch", "evictions")
+             "reused_tokens", "decode_tokens", "cow_copies", "max_batch", "evictions",
+             "prefill_chunks")
 
 
 @pytest.fixture(scope="module")
@@ -51,7 +52,8 @@ def test_library_scheduler_matches_the_model(lib, spec, policy, seed):
                   max_batch=rnd.choice([4, 16, 64]), pinning=rnd.choice([0, 1]),
                   eviction=rnd.choice([0, 1]), delta=rnd.choice([0, 7, 40]),
                   alpha=rnd.choice([1.0, 0.8]), beta=rnd.choice([0.5, 0.2]),
-                  breadth_share=rnd.choice([0.3, 0.6]), min_obs=rnd.choice([1, 8]))
+                  breadth_share=rnd.choice([0.3, 0.6]), min_obs=rnd.choice([1, 8]),
+                  max_step_tokens=rnd.choice([0, 0, 5, 100, 2048]))
         try:
             m, st, tr, bud = _both(lib, d, **kw)
         except ValueError:  # the pool is below the stages' minimum budgets
@@ -91,7 +93,8 @@ def test_bad_configurations_are_refused(lib):
                dict(policy=0, num_blocks=800, max_out=64, alpha=0.0),
                dict(policy=2, num_blocks=800, max_out=64, breadth_share=1.5),
                dict(policy=0, num_blocks=10, max_out=64),      # below the minimum budgets
-               dict(policy=0, num_blocks=800, max_out=8)):     # an output longer than max_out
+               dict(policy=0, num_blocks=800, max_out=8),      # an output longer than max_out
+               dict(policy=0, num_blocks=800, max_out=64, max_step_tokens=-1)):
         with pytest.raises(lib.PkvError) as e:
             lib.pkv_sched_run(lib.sched_config(**kw), *args)
         assert e.value.status == lib.PKV_ERR_INVALID_ARG

@@ -258,3 +258,47 @@ def test_prefixes_are_pinned_exactly_while_children_need_them(pinning):
     m.complete = complete
     m.run()
     assert tasks
+
+
+def test_chunked_prefill_worked_by_hand():
+    # task A: 10-token prompt, 3 output tokens; task B: 50-token prompt, 1 output token;
+    # budget 16 tokens per step, decodes first:
+    #   step 0: A prefills 10 (token 1), B 6      step 1: A decodes (token 2), B 15 (21)
+    #   step 2: A decodes (token 3: done), B 15 (36)   step 3: B 14 (50: token 1, done)
+    d = dict(fanout=[1], suffix=[[10, 50]], out_len=[[3, 1]], filtered=[[0, 0]])
+    m = run_schedule(Pipeline(**d), Config(ADAPTIVE, 64, max_out=8, static_bound=[8],
+                                           max_step_tokens=16))
+    outs = {e[3]: e[0] for e in m.trace if e[1] == EV_OUTPUT}
+    assert outs == {0: 2, 1: 3}
+    assert m.stats["prefill_chunks"] == 1 + 4 and m.stats["steps"] == 4
+    assert m.stats["prefill_tokens"] == 60 and m.stats["decode_tokens"] == 2
+
+
+@pytest.mark.parametrize("budget", [1, 7, 64, 512])
+def test_chunked_prefill_keeps_the_result_and_the_budget(budget):
+    d, pipe = small(PIPELINES[2], 20)
+    kw = dict(max_out=64, static_bound=[64] * pipe.S, max_batch=16)
+    ref = run_schedule(pipe, Config(ADAPTIVE, 1500, **kw))
+    m = SchedulerModel(pipe, Config(ADAPTIVE, 1500, max_step_tokens=budget, **kw))
+    per_step = []
+    commit = m.pool.commit
+    step_fn = m.engine_step
+
+    def counted_commit(sid, n):
+        per_step[-1] += n
+        return commit(sid, n)
+
+    def counted_step():
+        per_step.append(0)
+        return step_fn()
+
+    m.pool.commit = counted_commit
+    m.engine_step = counted_step
+    m.run()
+    assert max(per_step) <= budget
+    assert sorted(m.out) == sorted(ref.out) == surviving_outputs(d)
+    assert m.stats["prefill_tokens"] == ref.stats["prefill_tokens"]
+    assert m.stats["decode_tokens"] == ref.stats["decode_tokens"]
+    assert m.stats["misses"] == 0 and m.stats["retries"] == 0
+    assert m.stats["prefill_chunks"] >= ref.stats["prefill_chunks"]
+    assert all(u == 0 for u in m.used)
