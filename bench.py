@@ -75,8 +75,8 @@ def source_hash(*names):
 
 
 KERNEL_SOURCES = {
-    "prefill": ("prefill.hip", "device_utils.h"),
-    "decode": ("decode.hip", "device_utils.h"),
+    "prefill": ("prefill.hip", "prefill_impl.h", "device_utils.h"),
+    "decode": ("decode.hip", "decode_impl.h", "device_utils.h"),
     "append": ("kv_copy.hip", "device_utils.h"),
 }
 
@@ -397,6 +397,11 @@ def secondary(args, lib, torch):
            lambda: lib.pkv_decode_attention(pk, pv, bd.q, dd["tables"], sl, maxl, wl.scale,
                                             od, workspace=ws)]
     _, gpu, per = time_events(torch, stream, fns, steps, warm)
+    # the same set with prefill and decode fused into one mixed launch
+    fused = fns[:2] + [lambda: lib.pkv_mixed_attention(
+        pk, pv, wl.scale, bp.q, dp["tables"], dp["cached"], dp["cu"], dp["max_new"],
+        dp["max_total"], op, bd.q, dd["tables"], sl, maxl, od, workspace=ws)]
+    _, gpu_f, per_f = time_events(torch, stream, fused, steps, warm)
     flops = prefill_flops(bp.prefix_lens, bp.new_lens, wl.hq, wl.d)
     dbytes = decode_bytes(bd.prefix_lens + 1, wl.hq, wl.hkv, wl.d)
     abytes = append_bytes(Tp, wl.hkv, wl.d)
@@ -406,7 +411,9 @@ def secondary(args, lib, torch):
                       "prefill_frac_mfma": flops / per[2] / 1e12 / PEAK_BF16_TFLOPS,
                       "decode_ms": per[3] * 1e3, "decode_GB_s": dbytes / per[3] / 1e9,
                       "decode_frac_hbm": dbytes / per[3] / 1e9 / PEAK_HBM_GBS,
-                      "set_ms": gpu * 1e3, "sequences_per_s": (bp.n_seqs + bd.n_seqs) / gpu}
+                      "set_ms": gpu * 1e3, "sequences_per_s": (bp.n_seqs + bd.n_seqs) / gpu,
+                      "mixed_launch_ms": per_f[2] * 1e3, "set_with_mixed_launch_ms": gpu_f * 1e3,
+                      "sequences_per_s_mixed_launch": (bp.n_seqs + bd.n_seqs) / gpu_f}
     del wl, pk, pv
     torch.cuda.empty_cache()
 
@@ -567,6 +574,34 @@ def profile_copy(args, torch):
                       "GB_s": 2 * n / per[0] / 1e9}), flush=True)
 
 
+def profile_mixed(args, lib, torch, wl):
+    """The mixed launch (prefill and decode batches of one workload fused) `steps` times."""
+    from tests.gpu_util import i32
+    kinds = [b.kind for b, _ in wl.batches]
+    if kinds != ["prefill", "decode"]:
+        raise SystemExit(f"{wl.spec.name} is not a prefill + decode workload")
+    (bp, _), (bd, _) = wl.batches
+    dp, dd = wl.dev
+    pk, pv = wl.case.pool_k, wl.case.pool_v
+    lib.pkv_kv_append(pk, pv, bp.k_new, bp.v_new, dp["tables"], dp["cached"], dp["cu"],
+                      dp["max_new"])
+    lib.pkv_kv_append(pk, pv, bd.k_new, bd.v_new, dd["tables"], dd["cached"], dd["cu"], 1)
+    op = torch.empty((bp.total_new, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
+    od = torch.empty((bd.n_seqs, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
+    sl = i32(bd.prefix_lens + 1)
+    maxl = int(bd.prefix_lens.max()) + 1
+    ws = lib.alloc_workspace(lib.pkv_decode_workspace_bytes(bd.n_seqs, wl.hq, wl.hkv, wl.d,
+                                                            maxl))
+    fn = lambda: lib.pkv_mixed_attention(pk, pv, wl.scale, bp.q, dp["tables"], dp["cached"],
+                                         dp["cu"], dp["max_new"], dp["max_total"], op, bd.q,
+                                         dd["tables"], sl, maxl, od, workspace=ws)
+    stream = torch.cuda.current_stream()
+    _, gpu, per = time_events(torch, stream, [fn], args.steps, args.warmup)
+    print(json.dumps({"workload": wl.spec.name, "kernel": "mixed",
+                      "launches": args.steps + args.warmup, "avg_ms": per[0] * 1e3}),
+          flush=True)
+
+
 def profile_kernel(args, lib, torch):
     """Launch one kernel of the hot path `steps` times on one workload (for rocprofv3)."""
     import workloads as W
@@ -574,6 +609,8 @@ def profile_kernel(args, lib, torch):
         return profile_copy(args, torch)
     spec = W.BY_NAME[args.workload]
     wl = Workload(spec, lib, torch)
+    if args.profile_kernel == "mixed":
+        return profile_mixed(args, lib, torch, wl)
     kind = "decode" if args.profile_kernel == "decode" else "prefill"
     bi = [k for k, (b, _) in enumerate(wl.batches) if b.kind == kind]
     if not bi:
@@ -616,7 +653,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--profile-kernel", choices=("prefill", "decode", "append", "copy"))
+    ap.add_argument("--profile-kernel", choices=("prefill", "decode", "append", "copy", "mixed"))
     ap.add_argument("--workload", default="llama3_8b_prefix_reuse_prefill")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:

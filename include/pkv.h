@@ -281,6 +281,26 @@ size_t pkv_decode_workspace_bytes(int32_t num_seqs, int32_t num_q_heads, int32_t
 pkv_status pkv_copy_blocks(const pkv_paged_kv* kv, const int32_t* pairs, int32_t num_pairs,
                            void* stream);
 
+/* Mixed prefill + decode (the mixed batch of a serving step: downstream operators
+ * prefilling their suffixes while other tuples decode). Identical results, bit for bit, to
+ * pkv_prefill_attention on the prefill arguments (q .. lse, as there; no workspace) followed
+ * by pkv_decode_attention on the decode arguments (dq .. d_lse, with workspace and
+ * workspace_bytes as there), with the same num_q_heads and scale; either batch may be empty
+ * (zero sequences or zero new tokens). Both read the same pool, so the new tokens of both
+ * batches must have been appended before the call. One fused kernel runs prefill workgroups
+ * (matrix-core bound) and decode workgroups (HBM bound) side by side on every compute unit,
+ * between the decode's ordering and merge kernels. The two batches' outputs must not
+ * overlap. Errors are those of the two calls. */
+pkv_status pkv_mixed_attention(const pkv_paged_kv* kv, int32_t num_q_heads, float scale,
+                               const void* q, const int32_t* block_tables, int32_t max_blocks,
+                               const int32_t* cached_lens, const int32_t* cu_new_lens,
+                               int32_t num_seqs, int32_t total_new, int32_t max_new_len,
+                               int32_t max_total_len, void* out, float* lse, const void* dq,
+                               const int32_t* d_block_tables, int32_t d_max_blocks,
+                               const int32_t* seq_lens, int32_t d_num_seqs,
+                               int32_t max_seq_len, void* d_out, float* d_lse,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
 /* Paged gather (test support): copies the first lens[i] tokens of every sequence out of the
  * pool into contiguous k_out / v_out, bf16 [sum lens][num_kv_heads][head_dim], sequence i
  * starting at row cu_lens[i] (int32 [num_seqs + 1]). Bit-exact. max_len (host) >= every

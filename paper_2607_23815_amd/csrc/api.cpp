@@ -57,6 +57,81 @@ pkv_status launched(hipError_t err, const char* fn) {
   return ok();
 }
 
+// Argument checks of a prefill batch (prefill and mixed calls); *empty when there is nothing
+// to compute.
+pkv_status check_prefill(const KvView& view, const char* fn, const void* q, int32_t num_q_heads,
+                         const int32_t* block_tables, int32_t max_blocks,
+                         const int32_t* cached_lens, const int32_t* cu_new_lens,
+                         int32_t num_seqs, int32_t total_new, int32_t max_new_len,
+                         int32_t max_total_len, float scale, const void* out,
+                         const void* workspace, size_t workspace_bytes, bool* empty) {
+  const std::string f(fn);
+  *empty = false;
+  if (num_q_heads <= 0 || num_q_heads % view.hkv != 0)
+    return fail(PKV_ERR_UNSUPPORTED_SHAPE,
+                f + ": num_q_heads must be a positive multiple of num_kv_heads");
+  if (num_seqs < 0 || total_new < 0 || max_new_len < 0 || max_total_len < 0 || max_blocks < 0)
+    return fail(PKV_ERR_INVALID_ARG, f + ": negative size");
+  if (num_seqs == 0 || total_new == 0) {
+    *empty = true;
+    return ok();
+  }
+  if (q == nullptr || out == nullptr || block_tables == nullptr || cached_lens == nullptr ||
+      cu_new_lens == nullptr)
+    return fail(PKV_ERR_INVALID_ARG, f + ": NULL pointer");
+  if (!aligned16(q) || !aligned16(out))
+    return fail(PKV_ERR_INVALID_ARG, f + ": q / out must be 16-byte aligned");
+  if (max_new_len == 0 || max_total_len < max_new_len || max_blocks == 0)
+    return fail(PKV_ERR_INVALID_ARG,
+                f + ": need 0 < max_new_len <= max_total_len, max_blocks > 0");
+  if ((int64_t)max_blocks * kSupportedBlockSize < max_total_len)
+    return fail(PKV_ERR_INVALID_ARG, f + ": max_total_len exceeds max_blocks * block_size");
+  if (!(scale > 0.f)) return fail(PKV_ERR_INVALID_ARG, f + ": scale <= 0");
+  if (num_seqs > kMaxGridZ)
+    return fail(PKV_ERR_INVALID_ARG, f + ": more than 65535 sequences");
+  const size_t need = pkv_prefill_workspace_bytes(num_seqs, total_new, num_q_heads, view.hkv,
+                                                  view.head_dim, max_new_len, max_total_len);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need))
+    return fail(PKV_ERR_INVALID_ARG, f + ": workspace too small");
+  return ok();
+}
+
+// Argument checks of a decode batch (decode and mixed calls).
+pkv_status check_decode(const KvView& view, const char* fn, const void* q, int32_t num_q_heads,
+                        const int32_t* block_tables, int32_t max_blocks,
+                        const int32_t* seq_lens, int32_t num_seqs, int32_t max_seq_len,
+                        float scale, const void* out, const void* workspace,
+                        size_t workspace_bytes, bool* empty) {
+  const std::string f(fn);
+  *empty = false;
+  if (num_q_heads <= 0 || num_q_heads % view.hkv != 0 || num_q_heads / view.hkv > 16)
+    return fail(PKV_ERR_UNSUPPORTED_SHAPE,
+                f + ": num_q_heads must be a multiple of num_kv_heads, with at most 16 query "
+                    "heads per kv head");
+  if (num_seqs < 0 || max_seq_len < 0 || max_blocks < 0)
+    return fail(PKV_ERR_INVALID_ARG, f + ": negative size");
+  if (num_seqs == 0) {
+    *empty = true;
+    return ok();
+  }
+  if (q == nullptr || out == nullptr || block_tables == nullptr || seq_lens == nullptr)
+    return fail(PKV_ERR_INVALID_ARG, f + ": NULL pointer");
+  if (!aligned16(q) || !aligned16(out))
+    return fail(PKV_ERR_INVALID_ARG, f + ": q / out must be 16-byte aligned");
+  if (max_seq_len == 0 || max_blocks == 0)
+    return fail(PKV_ERR_INVALID_ARG, f + ": max_seq_len, max_blocks must be > 0");
+  if ((int64_t)max_blocks * kSupportedBlockSize < max_seq_len)
+    return fail(PKV_ERR_INVALID_ARG, f + ": max_seq_len exceeds max_blocks * block_size");
+  if (!(scale > 0.f)) return fail(PKV_ERR_INVALID_ARG, f + ": scale <= 0");
+  const size_t need = decode_workspace_bytes(num_seqs, num_q_heads, view.hkv, view.head_dim,
+                                             max_seq_len);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need || !aligned16(workspace)))
+    return fail(PKV_ERR_INVALID_ARG,
+                f + ": workspace missing, too small or not 16-byte aligned "
+                    "(see pkv_decode_workspace_bytes)");
+  return ok();
+}
+
 }  // namespace
 }  // namespace pkv
 
@@ -114,30 +189,11 @@ pkv_status pkv_prefill_attention(const pkv_paged_kv* kv, const void* q, int32_t 
   KvView view;
   pkv_status st = check_kv(kv, fn, &view);
   if (st != PKV_OK) return st;
-  if (num_q_heads <= 0 || num_q_heads % view.hkv != 0)
-    return fail(PKV_ERR_UNSUPPORTED_SHAPE,
-                "pkv_prefill_attention: num_q_heads must be a positive multiple of num_kv_heads");
-  if (num_seqs < 0 || total_new < 0 || max_new_len < 0 || max_total_len < 0 || max_blocks < 0)
-    return fail(PKV_ERR_INVALID_ARG, "pkv_prefill_attention: negative size");
-  if (num_seqs == 0 || total_new == 0) return ok();
-  if (q == nullptr || out == nullptr || block_tables == nullptr || cached_lens == nullptr ||
-      cu_new_lens == nullptr)
-    return fail(PKV_ERR_INVALID_ARG, "pkv_prefill_attention: NULL pointer");
-  if (!aligned16(q) || !aligned16(out))
-    return fail(PKV_ERR_INVALID_ARG, "pkv_prefill_attention: q / out must be 16-byte aligned");
-  if (max_new_len == 0 || max_total_len < max_new_len || max_blocks == 0)
-    return fail(PKV_ERR_INVALID_ARG,
-                "pkv_prefill_attention: need 0 < max_new_len <= max_total_len, max_blocks > 0");
-  if ((int64_t)max_blocks * kSupportedBlockSize < max_total_len)
-    return fail(PKV_ERR_INVALID_ARG,
-                "pkv_prefill_attention: max_total_len exceeds max_blocks * block_size");
-  if (!(scale > 0.f)) return fail(PKV_ERR_INVALID_ARG, "pkv_prefill_attention: scale <= 0");
-  if (num_seqs > kMaxGridZ)
-    return fail(PKV_ERR_INVALID_ARG, "pkv_prefill_attention: more than 65535 sequences");
-  const size_t need = pkv_prefill_workspace_bytes(num_seqs, total_new, num_q_heads, view.hkv,
-                                                  view.head_dim, max_new_len, max_total_len);
-  if (need > 0 && (workspace == nullptr || workspace_bytes < need))
-    return fail(PKV_ERR_INVALID_ARG, "pkv_prefill_attention: workspace too small");
+  bool empty = false;
+  st = check_prefill(view, fn, q, num_q_heads, block_tables, max_blocks, cached_lens,
+                     cu_new_lens, num_seqs, total_new, max_new_len, max_total_len, scale, out,
+                     workspace, workspace_bytes, &empty);
+  if (st != PKV_OK || empty) return st;
   return launched(launch_prefill(view, static_cast<const uint16_t*>(q), num_q_heads,
                                  block_tables, max_blocks, cached_lens, cu_new_lens, num_seqs,
                                  max_new_len, scale, static_cast<uint16_t*>(out), lse,
@@ -162,33 +218,58 @@ pkv_status pkv_decode_attention(const pkv_paged_kv* kv, const void* q, int32_t n
   KvView view;
   pkv_status st = check_kv(kv, fn, &view);
   if (st != PKV_OK) return st;
-  if (num_q_heads <= 0 || num_q_heads % view.hkv != 0 || num_q_heads / view.hkv > 16)
-    return fail(PKV_ERR_UNSUPPORTED_SHAPE,
-                "pkv_decode_attention: num_q_heads must be a multiple of num_kv_heads, with "
-                "at most 16 query heads per kv head");
-  if (num_seqs < 0 || max_seq_len < 0 || max_blocks < 0)
-    return fail(PKV_ERR_INVALID_ARG, "pkv_decode_attention: negative size");
-  if (num_seqs == 0) return ok();
-  if (q == nullptr || out == nullptr || block_tables == nullptr || seq_lens == nullptr)
-    return fail(PKV_ERR_INVALID_ARG, "pkv_decode_attention: NULL pointer");
-  if (!aligned16(q) || !aligned16(out))
-    return fail(PKV_ERR_INVALID_ARG, "pkv_decode_attention: q / out must be 16-byte aligned");
-  if (max_seq_len == 0 || max_blocks == 0)
-    return fail(PKV_ERR_INVALID_ARG, "pkv_decode_attention: max_seq_len, max_blocks must be > 0");
-  if ((int64_t)max_blocks * kSupportedBlockSize < max_seq_len)
-    return fail(PKV_ERR_INVALID_ARG,
-                "pkv_decode_attention: max_seq_len exceeds max_blocks * block_size");
-  if (!(scale > 0.f)) return fail(PKV_ERR_INVALID_ARG, "pkv_decode_attention: scale <= 0");
-  const size_t need = decode_workspace_bytes(num_seqs, num_q_heads, view.hkv, view.head_dim,
-                                             max_seq_len);
-  if (need > 0 && (workspace == nullptr || workspace_bytes < need || !aligned16(workspace)))
-    return fail(PKV_ERR_INVALID_ARG,
-                "pkv_decode_attention: workspace missing, too small or not 16-byte aligned "
-                "(see pkv_decode_workspace_bytes)");
+  bool empty = false;
+  st = check_decode(view, fn, q, num_q_heads, block_tables, max_blocks, seq_lens, num_seqs,
+                    max_seq_len, scale, out, workspace, workspace_bytes, &empty);
+  if (st != PKV_OK || empty) return st;
   return launched(launch_decode(view, static_cast<const uint16_t*>(q), num_q_heads,
                                 block_tables, max_blocks, seq_lens, num_seqs, max_seq_len, scale,
                                 static_cast<uint16_t*>(out), lse, workspace,
                                 static_cast<hipStream_t>(stream)),
+                  fn);
+}
+
+pkv_status pkv_mixed_attention(const pkv_paged_kv* kv, int32_t num_q_heads, float scale,
+                               const void* q, const int32_t* block_tables, int32_t max_blocks,
+                               const int32_t* cached_lens, const int32_t* cu_new_lens,
+                               int32_t num_seqs, int32_t total_new, int32_t max_new_len,
+                               int32_t max_total_len, void* out, float* lse, const void* dq,
+                               const int32_t* d_block_tables, int32_t d_max_blocks,
+                               const int32_t* seq_lens, int32_t d_num_seqs,
+                               int32_t max_seq_len, void* d_out, float* d_lse,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  const char* fn = "pkv_mixed_attention";
+  KvView view;
+  pkv_status st = check_kv(kv, fn, &view);
+  if (st != PKV_OK) return st;
+  bool no_prefill = false, no_decode = false;
+  st = check_prefill(view, fn, q, num_q_heads, block_tables, max_blocks, cached_lens,
+                     cu_new_lens, num_seqs, total_new, max_new_len, max_total_len, scale, out,
+                     nullptr, 0, &no_prefill);
+  if (st != PKV_OK) return st;
+  st = check_decode(view, fn, dq, num_q_heads, d_block_tables, d_max_blocks, seq_lens,
+                    d_num_seqs, max_seq_len, scale, d_out, workspace, workspace_bytes,
+                    &no_decode);
+  if (st != PKV_OK) return st;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (no_prefill && no_decode) return ok();
+  if (no_decode)
+    return launched(launch_prefill(view, static_cast<const uint16_t*>(q), num_q_heads,
+                                   block_tables, max_blocks, cached_lens, cu_new_lens, num_seqs,
+                                   max_new_len, scale, static_cast<uint16_t*>(out), lse, s),
+                    fn);
+  if (no_prefill)
+    return launched(launch_decode(view, static_cast<const uint16_t*>(dq), num_q_heads,
+                                  d_block_tables, d_max_blocks, seq_lens, d_num_seqs,
+                                  max_seq_len, scale, static_cast<uint16_t*>(d_out), d_lse,
+                                  workspace, s),
+                    fn);
+  return launched(launch_mixed(view, num_q_heads, scale, static_cast<const uint16_t*>(q),
+                               block_tables, max_blocks, cached_lens, cu_new_lens, num_seqs,
+                               max_new_len, static_cast<uint16_t*>(out), lse,
+                               static_cast<const uint16_t*>(dq), d_block_tables, d_max_blocks,
+                               seq_lens, d_num_seqs, max_seq_len, static_cast<uint16_t*>(d_out),
+                               d_lse, workspace, s),
                   fn);
 }
 

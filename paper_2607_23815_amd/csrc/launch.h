@@ -39,10 +39,38 @@ hipError_t launch_prefill(const KvView& kv, const uint16_t* q, int32_t hq,
 int32_t decode_split_keys(int32_t num_seqs, int32_t hkv, int32_t max_seq_len);
 size_t decode_workspace_bytes(int32_t num_seqs, int32_t hq, int32_t hkv, int32_t head_dim,
                               int32_t max_seq_len);
+// The pieces of a decode launch, shared with the mixed launch: the split plan and the
+// workspace layout (the sequence order, then the splits' partial results), the ordering
+// kernel, and the merge of partial results (nothing when no sequence splits).
+struct DecodePlan {
+  int32_t split, max_splits;
+  int32_t* order;
+  float* ws_o;
+  float* ws_ml;
+  int64_t items;  // (sequence, kv head, split) work items
+};
+DecodePlan decode_plan(const KvView& kv, int32_t hq, int32_t num_seqs, int32_t max_seq_len,
+                       void* workspace);
+hipError_t launch_decode_order(const int32_t* seq_lens, int32_t num_seqs, int32_t* order,
+                               hipStream_t stream);
+hipError_t launch_decode_merge(const KvView& kv, const DecodePlan& p, int32_t hq,
+                               const int32_t* seq_lens, int32_t num_seqs, uint16_t* out,
+                               float* lse, hipStream_t stream);
 hipError_t launch_decode(const KvView& kv, const uint16_t* q, int32_t hq,
                          const int32_t* block_tables, int32_t max_blocks,
                          const int32_t* seq_lens, int32_t num_seqs, int32_t max_seq_len,
                          float scale, uint16_t* out, float* lse, void* workspace,
                          hipStream_t stream);
+
+// Mixed launch: a prefill batch (arguments as launch_prefill) and a decode batch (d_*, as
+// launch_decode, with its workspace) in one fused kernel between the decode's ordering
+// kernel and its merge. Both batches must be non-empty.
+hipError_t launch_mixed(const KvView& kv, int32_t hq, float scale, const uint16_t* q,
+                        const int32_t* block_tables, int32_t max_blocks,
+                        const int32_t* cached_lens, const int32_t* cu_new_lens, int32_t num_seqs,
+                        int32_t max_new_len, uint16_t* out, float* lse, const uint16_t* dq,
+                        const int32_t* d_block_tables, int32_t d_max_blocks,
+                        const int32_t* seq_lens, int32_t d_num_seqs, int32_t max_seq_len,
+                        uint16_t* d_out, float* d_lse, void* workspace, hipStream_t stream);
 
 }  // namespace pkv

@@ -1,83 +1,14 @@
-// Prefix-reuse paged prefill attention for gfx950.
-//
-// A downstream operator's prefill computes attention only for its N new tokens; the keys are
-// the sequence's cached prefix (left in the pool by the upstream operator) followed by the new
-// tokens, all read through the block table. New token j sees keys 0 .. P + j.
-//
-// Work item = (sequence, kv head, tile of 32 x kWaves query columns). A column is one (new token,
-// query head) pair of the kv head's group, token-major, so the g = Hq/Hkv heads that share
-// the kv head are packed into the matrix-core M dimension and every K/V byte staged in LDS
-// serves all of them. The workgroup has kWaves waves (4: two independent workgroups per
-// compute unit overlap each other's stalls) of 32 columns each and walks the keys in tiles
-// of 64 (four 16-token blocks):
-//   1. K and V tiles are staged in LDS (double-buffered: the next tile's global loads are in
-//      flight while the current tile is multiplied). Staging is a 16-byte copy of whole pool
-//      slabs with a swizzle on the 16-byte unit index, so the matrix-core operand reads below
-//      hit distinct LDS banks.
-//   2. Scores S^T[64 keys][32 cols] = K . Q^T with v_mfma_f32_32x32x16_bf16; Q stays in
-//      registers for the whole work item.
-//   3. Online softmax in the base-2 domain (scale * log2 e folded in fp32). Each lane owns one
-//      column, so the running max, sum and output rescale are lane-local except for one
-//      exchange with the lane 32 apart that holds the column's other keys.
-//   4. O^T[D][32 cols] += V^T . P^T, again 32x32x16, with P^T taken straight from the score
-//      registers (rounded to bf16). For this to need no data movement, score row m of the
-//      32-key half-tile is loaded with key sigma(m), sigma swapping bits 2 and 3 of the key
-//      index; then the 8 keys a lane contributes to each value-product step are 8
-//      consecutive slots, i.e. one 16-byte chunk of the dim-major V slab.
-// Masking is by selection (scores to -inf), applied only to tiles that reach past some
-// column's last visible key; V slots past the sequence end are zeroed while staging, so stale
-// bits (NaN included) never meet a zero weight inside the matrix core.
-#include <math.h>
-
-#include <type_traits>
-
-#include "device_utils.h"
+// Prefix-reuse paged prefill attention for gfx950: the prefill-only launch. The workgroup
+// body (work items, staging, the matrix-core products and the online softmax) is in
+// prefill_impl.h.
 #include "launch.h"
+#include "prefill_impl.h"
 
 namespace pkv {
 namespace {
 
-constexpr int kWaves = 4;             // waves per workgroup
-constexpr int kThreads = 64 * kWaves;
-constexpr int kCols = 32 * kWaves;    // query columns per workgroup (32 per wave)
-constexpr int kSlabWaves = kWaves / 4;  // waves staging each of a tile's four block slabs
-constexpr int kKeys = 64;   // keys per tile (4 blocks)
-
-// Wait until every global load this thread issued has completed (vmcnt = 0; the other
-// counters left at their maxima), so its direct-to-LDS loads have been written.
-__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
-
-// The value held by the lane 32 apart (lanes l and l ^ 32 hold the two key halves of one
-// column): v_permlane32_swap exchanges the upper half of one register with the lower half of
-// another, so swapping a register with a copy of itself gives every lane its partner's value.
-__device__ __forceinline__ float swap_halves(float x) {
-  const uint32_t u = __float_as_uint(x);
-  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-  // lanes < 32 find the partner in the second result, lanes >= 32 in the first
-  return __uint_as_float((threadIdx.x & 32) ? r[0] : r[1]);
-}
-
-// sigma: swap bits 2 and 3 of a key index within a 16-key block (an involution)
-__device__ __forceinline__ int swap23(int s) {
-  return (s & ~0xC) | ((s & 8) >> 1) | ((s & 4) << 1);
-}
-
 template <int D>
-struct PrefillSmem {
-  static constexpr int SLAB = D * kBlockSize;  // elements per block slab
-  uint16_t k[2][4 * SLAB];
-  uint16_t v[2][4 * SLAB];
-};
-
-// Rescale the running output only when a column's maximum grows by more than this many
-// powers of two; otherwise keep the stale maximum (weights then stay below 2^8, exact in the
-// normalisation). After the first tiles the maximum of N(0,1) scores hardly moves, so the
-// 64 accumulator multiplies per tile are almost always skipped.
-constexpr float kRescaleThreshold = 8.0f;
-constexpr float kRescaleLimit = 256.0f;  // 2^kRescaleThreshold
-
-template <int D>
-__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads),
+__global__ __attribute__((amdgpu_flat_work_group_size(pre::kThreads, pre::kThreads),
                           amdgpu_waves_per_eu(2, 2)))
 void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
                     const uint16_t* __restrict__ v_cache, const int32_t* __restrict__ block_tables,
@@ -85,373 +16,9 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
                     const int32_t* __restrict__ cu_new_lens, int32_t num_seqs, int32_t hq,
                     int32_t hkv, int32_t num_blocks, int32_t qtiles, float scale_log2,
                     uint16_t* __restrict__ out, float* __restrict__ lse) {
-  constexpr int SLAB = D * kBlockSize;
-  constexpr int UNITS = SLAB / 8;        // 16-byte units per block slab
-  constexpr int LPT = 4 * UNITS / kThreads;  // 16-byte units per thread per tile (K or V)
-  constexpr int KK = D / 16;             // k-steps of the score product
-  constexpr int DB = D / 32;             // 32-dim blocks of the value product
-  __shared__ __align__(16) PrefillSmem<D> sm;
-
-  // XCD-aware mapping: workgroup id b runs on XCD b % 8. The unit that must stay on one XCD
-  // is a (sequence, kv head) group -- its query tiles read the same K/V and share that XCD's
-  // L2 when they run together -- so groups are dealt to XCDs round-robin (group index mod 8)
-  // and each XCD walks its groups in order, query tiles longest first. With 8 kv heads every
-  // XCD receives one kv head of every sequence: equal work per XCD, whatever the lengths.
-  const int xcd = blockIdx.x & 7;
-  const int pos = blockIdx.x >> 3;                 // position in this XCD's list
-  const int group = (pos / qtiles) * 8 + xcd;      // (sequence, kv head) group index
-  const int qt = qtiles - 1 - pos % qtiles;        // longest (last) query tile first
-  if (group >= num_seqs * hkv) return;
-  const int kvh = group % hkv;
-  const int i = group / hkv;
-
-  // The first table chunk (entry `lane` of the sequence's row, and entry 0) is fetched
-  // before the lengths: its address depends on the sequence only, so the two loads overlap.
-  const int32_t* table = block_tables + (size_t)i * max_blocks;
-  const int32_t t_first = table[0];
-  const int32_t t_lane = (int)(threadIdx.x & 63) < max_blocks ? table[threadIdx.x & 63] : -1;
-
-  const int g = hq / hkv;
-  const int p = cached_lens[i];
-  const int row0 = cu_new_lens[i];
-  const int n = cu_new_lens[i + 1] - row0;
-  const int ncols = n * g;
-  const int col0 = qt * kCols;
-  if (col0 >= ncols) return;
-  const int len = p + n;
-
-  const int tid = threadIdx.x;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
-  const int lane = tid & 63;
-  const int lc = lane & 31;
-  const int hh = lane >> 5;
-
-  const int gcol = col0 + wave * 32 + lc;
-  const bool col_ok = gcol < ncols;
-  const int j = col_ok ? gcol / g : n - 1;
-  const int head = kvh * g + gcol % g;
-  const int lim = p + j;  // last key this column sees
-
-  const int jmax = min(n - 1, (col0 + kCols - 1) / g);
-  const int nkeys = p + jmax + 1;
-  const int ntiles = (nkeys + kKeys - 1) / kKeys;
-  const int wcol0 = col0 + wave * 32;
-  const int wj_lo = min(wcol0 / g, n - 1);         // earliest token among the wave's columns
-  const bool wave_live = wcol0 < ncols;            // the wave has at least one real column
-
-  bf16x8 qf[KK];  // Q fragments, loaded in the prologue
-  f32x16 o[DB];
-#pragma unroll
-  for (int db = 0; db < DB; ++db)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
-  float m = -INFINITY;
-  float lpart = 0.f;
-
-  const size_t head_off = (size_t)kvh * SLAB;
-  // stand-in for blocks past the sequence: its first block (len >= 1, so it owns one)
-  const int32_t blk_first = (t_first >= 0 && t_first < num_blocks) ? t_first : 0;
-
-  // ---- staging: direct global -> LDS 16-byte loads. Wave w stages block w % 4 of every
-  // tile, sharing it with the other kWaves / 4 - 1 waves of that block: its load k fills LDS
-  // units 64 (part * WLOADS + k) + lane of that block's slab (with four waves, the whole
-  // 4 KB slab at head_dim 128 in four loads). The bank swizzle is applied on the global side: LDS K unit
-  // c*16 + t holds global unit c*16 + swap23(t), LDS V unit 2d + t holds global unit
-  // 2d + (t ^ ((d >> 3) & 1)); with these, the 16 lanes the LDS serves per cycle read 16
-  // distinct 16-byte bank groups. ----
-  constexpr int WLOADS = UNITS / 64 / kSlabWaves;  // loads per wave per block slab
-  const int slab = wave & 3;                       // the block of the tile this wave stages
-  const int part = wave >> 2;                      // which WLOADS loads of that slab
-  int kofs[WLOADS], vofs[WLOADS];        // per-lane element offsets within a block slab
-#pragma unroll
-  for (int k = 0; k < WLOADS; ++k) {
-    const int pos = (part * WLOADS + k) * 64 + lane;
-    const int c = pos >> 4;
-    kofs[k] = (c * 16 + swap23(pos & 15)) * 8;
-    const int d = pos >> 1;
-    vofs[k] = (2 * d + ((pos & 1) ^ ((d >> 3) & 1))) * 8;
-  }
-  // Block-table entries through a per-wave register table: lane l of a chunk holds entry
-  // 64 c + l, already checked (entries past the sequence, past the table or out of the pool
-  // are replaced by the sequence's first block: finite data, masked or zeroed before use).
-  // A chunk covers 16 tiles; the K and V streams keep one chunk each.
-  auto load_chunk = [&](int c) {
-    const int e = c * 64 + lane;
-    int v = blk_first;
-    if (e < max_blocks && e * kBlockSize < len) {
-      const int t = table[e];
-      v = (t >= 0 && t < num_blocks) ? t : blk_first;
-    }
-    return v;
-  };
-  int kchunk = (lane * kBlockSize < len && t_lane >= 0 && t_lane < num_blocks) ? t_lane
-                                                                              : blk_first;
-  int kchunk_id = 0;
-  int vchunk = kchunk, vchunk_id = 0;
-  auto block_of = [&](int& chunk, int& chunk_id, int kt) {
-    const int e = kt * 4 + slab;  // the block of tile kt this wave stages
-    const int c = e >> 6;
-    if (c != chunk_id) {
-      chunk = load_chunk(c);
-      chunk_id = c;
-    }
-    return __builtin_amdgcn_readlane(chunk, e & 63);
-  };
-  // One slab = one buffer resource (base = the slab, 4 KB, bounds-checked by the hardware).
-  auto issue = [&](const uint16_t* cache, uint16_t* dst, const int (&ofs)[WLOADS], int blk) {
-    const uint16_t* src = cache + (size_t)blk * hkv * SLAB + head_off;
-#pragma unroll
-    for (int k = 0; k < WLOADS; ++k)
-      lds_load16(src, SLAB * 2, ofs[k] * 2, dst + slab * SLAB + (part * WLOADS + k) * 512);
-  };
-  auto issue_k = [&](int kt, int buf) {
-    issue(k_cache, sm.k[buf], kofs, block_of(kchunk, kchunk_id, kt));
-  };
-  auto issue_v = [&](int kt, int buf) {
-    issue(v_cache, sm.v[buf], vofs, block_of(vchunk, vchunk_id, kt));
-  };
-
-  // lane-constant LDS read offsets (elements)
-  const int kread = (lc >> 4) * SLAB + (hh * 16 + (lc & 15)) * 8;
-  const int vread = (2 * lc + (hh ^ ((lc >> 3) & 1))) * 8;
-
-  // scores S^T of the K tile in buffer kbuf, both 32-key halves (two independent chains)
-  auto scores = [&](int kbuf, f32x16 (&sc)[2]) {
-    u32x4 ka[2][KK];
-#pragma unroll
-    for (int beta = 0; beta < 2; ++beta)
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk)
-        ka[beta][kk] = ld16(&sm.k[kbuf][kread + beta * 2 * SLAB + kk * 256]);
-#pragma unroll
-    for (int beta = 0; beta < 2; ++beta)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sc[beta][r] = 0.f;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk)
-#pragma unroll
-      for (int beta = 0; beta < 2; ++beta)
-        sc[beta] = mfma32(as_bf16x8(ka[beta][kk]), qf[kk], sc[beta]);
-  };
-
-  // register r of half-tile beta holds the score of key
-  // key0 + 32 beta + 16 (r/8) + 8 hh + 4 ((r/4) % 2) + r % 4
-  auto mask_tile = [&](int key0, f32x16 (&sc)[2]) {
-#pragma unroll
-    for (int beta = 0; beta < 2; ++beta)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = key0 + 32 * beta + 16 * (r >> 3) + 8 * hh + 4 * ((r >> 2) & 1) + (r & 3);
-        sc[beta][r] = key <= lim ? sc[beta][r] : -INFINITY;
-      }
-  };
-
-  // weights of one tile: P = 2^(scale_log2 * S - m) rounded to bf16 (the value-product
-  // operand), and the sum of the fp32 weights before rounding (each rounded weight is within
-  // a relative 2^-9 of its fp32 value, unbiased). The sum is kept in eight independent
-  // partial sums: a single accumulator would chain dependent adds through the block and
-  // stall the in-order issue that has to keep the matrix cores fed.
-  auto weights = [&](f32x16 (&sc)[2], bf16x8 (&pw)[2][2]) {
-    const float neg_m = -m;
-    float sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int beta = 0; beta < 2; ++beta)
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        u32x4 w;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float a = fast_exp2(__builtin_fmaf(sc[beta][8 * u + 2 * e], scale_log2, neg_m));
-          const float b = fast_exp2(__builtin_fmaf(sc[beta][8 * u + 2 * e + 1], scale_log2, neg_m));
-          w[e] = pack_bf16x2(a, b);
-          sum[2 * e] += a;
-          sum[2 * e + 1] += b;
-        }
-        pw[beta][u] = as_bf16x8(w);
-      }
-    return ((sum[0] + sum[1]) + (sum[2] + sum[3])) + ((sum[4] + sum[5]) + (sum[6] + sum[7]));
-  };
-  // value product of one tile: O^T += V^T P^T; step (beta, u) covers block 2 beta + u of the
-  // tile, lane group hh supplying slots 8 hh .. 8 hh + 7 of V^T row 32 db + lc
-  auto values = [&](int vbuf, const bf16x8 (&pw)[2][2]) {
-    const uint16_t* vt = sm.v[vbuf];
-#pragma unroll
-    for (int beta = 0; beta < 2; ++beta)
-#pragma unroll
-      for (int u = 0; u < 2; ++u)
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const u32x4 a = ld16(&vt[(2 * beta + u) * SLAB + vread + db * 512]);
-          o[db] = mfma32(as_bf16x8(a), pw[beta][u], o[db]);
-        }
-  };
-
-  // One step of the software pipeline, for tile kt. On entry cur holds the raw scores of
-  // tile kt and pprev the weights of tile kt-1 (when has_prev). One straight-line block
-  // then issues the score MFMAs of tile kt+1 (when has_next) and the value MFMAs of tile
-  // kt-1, interleaved with the softmax of tile kt, whose weights use the running maximum m
-  // speculatively: with the lazy rescale m almost never moves, and when some column's
-  // maximum does grow by more than the threshold (always on the first tile, m = -inf) a
-  // rare branch rescales the accumulator and recomputes the weights.
-  // LDS: step kt reads K(kt+1) from K buffer (kt+1)&1 and V(kt-1) from V buffer (kt-1)&1,
-  // and loads K(kt+2) into K buffer kt&1 and V(kt) into V buffer kt&1 -- the buffers whose
-  // last readers were in step kt-1, which the barrier at the top of step kt has retired
-  // (V(0) is loaded by the prologue, whose buffers are all free).
-  auto step = [&](auto has_prev, auto has_next, int kt, f32x16 (&cur)[2], f32x16 (&nxt)[2],
-                  bf16x8 (&pprev)[2][2], bf16x8 (&pcur)[2][2]) {
-    wait_vmem();
-    __syncthreads();  // K(kt+1) and V(kt-1) have landed; all waves are done with step kt-1
-    if (kt + 2 < ntiles) issue_k(kt + 2, kt & 1);
-    if constexpr (decltype(has_prev)::value) issue_v(kt, kt & 1);  // V(0): prologue
-    if (!wave_live) return;
-    const int key0 = kt * kKeys;
-    if (key0 + kKeys - 1 > p + wj_lo) mask_tile(key0, cur);
-
-    // ---- the straight-line block ----
-    if constexpr (decltype(has_next)::value) scores((kt + 1) & 1, nxt);
-    if constexpr (decltype(has_prev)::value) values((kt - 1) & 1, pprev);
-    float lnew = weights(cur, pcur);
-    // keep the speculative weights in this block: without a use here the compiler would sink
-    // their computation past the rare branch below (which overwrites them), out of reach of
-    // the interleave
-    asm volatile("" ::"v"(__builtin_bit_cast(u32x4, pcur[0][0])),
-                 "v"(__builtin_bit_cast(u32x4, pcur[0][1])),
-                 "v"(__builtin_bit_cast(u32x4, pcur[1][0])),
-                 "v"(__builtin_bit_cast(u32x4, pcur[1][1])), "v"(lnew));
-    if constexpr (decltype(has_next)::value && decltype(has_prev)::value) {
-      // interleave: fragment reads ahead, then each of the 32 MFMAs followed by the next
-      // fragment read and a slice of the softmax arithmetic
-      __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);    // 6 LDS reads
-#pragma unroll
-      for (int k = 0; k < 32; ++k) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
-        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // 4 VALU
-      }
-    }
-    // The running maximum only has to move when some weight of the tile exceeds 2^threshold,
-    // and then this lane's (non-negative) weight sum exceeds it too: test the sum, and only
-    // then find the tile's exact maximum (the first tile, where m = -inf, always does).
-    bool check = true;
-    if constexpr (decltype(has_prev)::value)
-      check = __builtin_amdgcn_ballot_w64(!(lnew <= kRescaleLimit)) != 0;
-    if (check) {
-      float mx = -INFINITY;
-#pragma unroll
-      for (int beta = 0; beta < 2; ++beta)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, cur[beta][r]);
-      mx = fmaxf(mx, swap_halves(mx)) * scale_log2;
-      const bool grow = mx > m + kRescaleThreshold;
-      if (__builtin_amdgcn_ballot_w64(grow)) {
-        const float m_new = grow ? mx : m;
-        const float alpha = fast_exp2(m - m_new);
-        m = m_new;
-        lpart *= alpha;
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-        lnew = weights(cur, pcur);
-      }
-    }
-    lpart += lnew;
-  };
-
-  // prologue: K(0), K(1) and V(0) (every buffer is free; their blocks are entries 0..7 of
-  // the first chunk), then Q, all under one wait; scores of tile 0
-  issue(k_cache, sm.k[0], kofs, __builtin_amdgcn_readlane(kchunk, slab));
-  if (ntiles > 1) issue(k_cache, sm.k[1], kofs, __builtin_amdgcn_readlane(kchunk, 4 + slab));
-  issue(v_cache, sm.v[0], vofs, __builtin_amdgcn_readlane(kchunk, slab));
-  // Q as the B operand of S^T = K Q^T: lane holds Q[column lc][16 kk + 8 hh .. +7]. A lane
-  // past the last column reads a valid row (token n - 1) and keeps zeros, so the loads are
-  // unconditional and the wait above counts them exactly.
-  {
-    const uint16_t* qrow = q + ((size_t)(row0 + j) * hq + head) * D + hh * 8;
-    u32x4 qv[KK];
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) qv[kk] = ld16(qrow + kk * 16);
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      const u32x4 zero = {0u, 0u, 0u, 0u};
-      qf[kk] = as_bf16x8(col_ok ? qv[kk] : zero);
-    }
-  }
-  wait_vmem();
-  __syncthreads();
-  f32x16 sa[2], sb[2];
-  bf16x8 pa[2][2], pb[2][2];
-  if (wave_live) scores(0, sa);
-  using yes = std::true_type;
-  using no = std::false_type;
-  // step kt consumes scores sa/sb alternately and writes weights pa/pb alternately
-  if (ntiles == 1) {
-    step(no(), no(), 0, sa, sb, pb, pa);
-  } else {
-    step(no(), yes(), 0, sa, sb, pb, pa);
-    int kt = 1;
-    for (; kt + 2 < ntiles; kt += 2) {
-      step(yes(), yes(), kt, sb, sa, pa, pb);
-      step(yes(), yes(), kt + 1, sa, sb, pb, pa);
-    }
-    if (kt + 1 < ntiles) {
-      step(yes(), yes(), kt, sb, sa, pa, pb);
-      step(yes(), no(), kt + 1, sa, sb, pb, pa);
-      kt += 2;
-    } else {
-      step(yes(), no(), kt, sb, sa, pa, pb);
-      kt += 1;
-    }
-    (void)kt;
-  }
-  // epilogue: V of the last tile (loaded by the last step) lands; where that tile reaches
-  // past the sequence, zero the V slots >= len (they may hold any bits); then its value
-  // product, with the weights in pa when ntiles is odd and in pb when it is even
-  {
-    const int kt = ntiles - 1;
-    wait_vmem();
-    __syncthreads();
-    if ((kt + 1) * kKeys > len) {
-      uint16_t* vt = sm.v[kt & 1];
-#pragma unroll
-      for (int k = 0; k < LPT; ++k) {
-        const int P = tid + kThreads * k;
-        const int bb = P / UNITS, pos = P % UNITS;
-        const int d = pos >> 1;
-        const int hf = (pos & 1) ^ ((d >> 3) & 1);
-        const int first = kt * kKeys + bb * kBlockSize + hf * 8;
-        const int keep = min(max(len - first, 0), 8);
-        if (keep < 8) {
-          u32x4 w = ld16(&vt[P * 8]);
-          uint32_t words[4] = {w[0], w[1], w[2], w[3]};
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (e >= keep) words[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
-          st16(&vt[P * 8], u32x4{words[0], words[1], words[2], words[3]});
-        }
-      }
-      __syncthreads();
-    }
-    if (wave_live) {
-      if (ntiles & 1) values(kt & 1, pa);
-      else values(kt & 1, pb);
-    }
-  }
-
-  const float l = lpart + swap_halves(lpart);
-  if (!col_ok) return;
-  const float inv = 1.f / l;
-  uint16_t* orow = out + ((size_t)(row0 + j) * hq + head) * D;
-#pragma unroll
-  for (int db = 0; db < DB; ++db)
-#pragma unroll
-    for (int a = 0; a < 4; ++a) {
-      // registers 4a .. 4a+3 hold dims 32 db + 8 a + 4 hh + 0..3
-      u32x2 w = {pack_bf16x2(o[db][4 * a + 0] * inv, o[db][4 * a + 1] * inv),
-                 pack_bf16x2(o[db][4 * a + 2] * inv, o[db][4 * a + 3] * inv)};
-      st8(orow + db * 32 + 8 * a + 4 * hh, w);
-    }
-  if (lse != nullptr && hh == 0) lse[(size_t)(row0 + j) * hq + head] = (m + log2f(l)) * kLn2;
+  pre::prefill_body<D>(q, k_cache, v_cache, block_tables, max_blocks, cached_lens, cu_new_lens,
+                       num_seqs, hq, hkv, num_blocks, qtiles, scale_log2, out, lse,
+                       blockIdx.x);
 }
 
 }  // namespace
@@ -461,19 +28,17 @@ hipError_t launch_prefill(const KvView& kv, const uint16_t* q, int32_t hq,
                           const int32_t* cached_lens, const int32_t* cu_new_lens,
                           int32_t num_seqs, int32_t max_new_len, float scale, uint16_t* out,
                           float* lse, hipStream_t stream) {
-  const int32_t g = hq / kv.hkv;
-  const int64_t qtiles = ((int64_t)max_new_len * g + kCols - 1) / kCols;
-  const int64_t groups = (int64_t)kv.hkv * num_seqs;
-  const int64_t items = (groups + 7) / 8 * 8 * qtiles;  // 8 XCD lists of equal length
-  if (items > INT32_MAX) return hipErrorInvalidValue;
-  const dim3 grid((unsigned)items);
+  const pre::PrefillGrid pg = pre::prefill_grid(hq, kv.hkv, num_seqs, max_new_len);
+  if (pg.items > INT32_MAX) return hipErrorInvalidValue;
+  const int64_t qtiles = pg.qtiles;
+  const dim3 grid((unsigned)pg.items);
   const float scale_log2 = scale * kLog2e;
   if (kv.head_dim == 128)
-    hipLaunchKernelGGL(prefill_kernel<128>, grid, dim3(kThreads), 0, stream, q, kv.k, kv.v,
+    hipLaunchKernelGGL(prefill_kernel<128>, grid, dim3(pre::kThreads), 0, stream, q, kv.k, kv.v,
                        block_tables, max_blocks, cached_lens, cu_new_lens, num_seqs, hq, kv.hkv,
                        kv.num_blocks, (int32_t)qtiles, scale_log2, out, lse);
   else
-    hipLaunchKernelGGL(prefill_kernel<64>, grid, dim3(kThreads), 0, stream, q, kv.k, kv.v,
+    hipLaunchKernelGGL(prefill_kernel<64>, grid, dim3(pre::kThreads), 0, stream, q, kv.k, kv.v,
                        block_tables, max_blocks, cached_lens, cu_new_lens, num_seqs, hq, kv.hkv,
                        kv.num_blocks, (int32_t)qtiles, scale_log2, out, lse);
   return hipGetLastError();

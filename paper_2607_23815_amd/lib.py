@@ -122,6 +122,11 @@ _SIGS = {
                                        c_int32, c_void_p, c_int32, c_int32, c_float, c_void_p,
                                        c_void_p, c_void_p, c_size_t, c_void_p]),
     "pkv_decode_workspace_bytes": (c_size_t, [c_int32] * 5),
+    "pkv_mixed_attention": (c_int32, [ctypes.POINTER(PagedKV), c_int32, c_float, c_void_p,
+                                      c_void_p, c_int32, c_void_p, c_void_p, c_int32, c_int32,
+                                      c_int32, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
+                                      c_int32, c_void_p, c_int32, c_int32, c_void_p, c_void_p,
+                                      c_void_p, c_size_t, c_void_p]),
     "pkv_gather_kv": (c_int32, [ctypes.POINTER(PagedKV), c_void_p, c_int32, c_void_p, c_void_p,
                                 c_int32, c_int32, c_void_p, c_void_p, c_void_p]),
 }
@@ -449,6 +454,36 @@ def pkv_decode_attention(k_cache, v_cache, q, block_tables, seq_lens, max_seq_le
         _dev_ptr(seq_lens, "seq_lens", torch.int32), b, int(max_seq_len), float(scale),
         _dev_ptr(out, "out", torch.bfloat16), _dev_ptr(lse, "lse", torch.float32),
         _dev_ptr(workspace, "workspace"), ws_bytes, _stream(stream)))
+
+
+def pkv_mixed_attention(k_cache, v_cache, scale: float,
+                        q, block_tables, cached_lens, cu_new_lens, max_new_len: int,
+                        max_total_len: int, out,
+                        dq, d_block_tables, seq_lens, max_seq_len: int, d_out,
+                        lse=None, d_lse=None, workspace=None, stream=None) -> None:
+    """A prefill batch (as pkv_prefill_attention) and a decode batch (as
+    pkv_decode_attention) in one fused launch."""
+    import torch
+    kv = paged_kv(k_cache, v_cache)
+    t, hq, d = q.shape
+    b = int(cached_lens.shape[0])
+    bd = int(seq_lens.shape[0])
+    if workspace is None:
+        workspace = alloc_workspace(pkv_decode_workspace_bytes(bd, hq, int(k_cache.shape[1]), d,
+                                                               int(max_seq_len)))
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(_lib.pkv_mixed_attention(
+        ctypes.byref(kv), hq, float(scale), _dev_ptr(q, "q", torch.bfloat16),
+        _dev_ptr(block_tables, "block_tables", torch.int32), int(block_tables.shape[1]),
+        _dev_ptr(cached_lens, "cached_lens", torch.int32),
+        _dev_ptr(cu_new_lens, "cu_new_lens", torch.int32), b, t, int(max_new_len),
+        int(max_total_len), _dev_ptr(out, "out", torch.bfloat16),
+        _dev_ptr(lse, "lse", torch.float32), _dev_ptr(dq, "dq", torch.bfloat16),
+        _dev_ptr(d_block_tables, "d_block_tables", torch.int32),
+        int(d_block_tables.shape[1]), _dev_ptr(seq_lens, "seq_lens", torch.int32), bd,
+        int(max_seq_len), _dev_ptr(d_out, "d_out", torch.bfloat16),
+        _dev_ptr(d_lse, "d_lse", torch.float32), _dev_ptr(workspace, "workspace"), ws_bytes,
+        _stream(stream)))
 
 
 def pkv_copy_blocks(k_cache, v_cache, pairs, stream=None) -> None:
