@@ -264,12 +264,18 @@ class Sched {
     filt_.assign(filtered, filtered + base);
     prefix_.assign((size_t)base, 0);
     for (int64_t k = 0; k < base; ++k) {
-      if (suffix_[k] < 0 || out_[k] < 1 || out_[k] > c_.max_out)
+      if (suffix_[k] < 0 || suffix_[k] > INT32_MAX / 4 || out_[k] < 1 || out_[k] > c_.max_out)
         return pkv::fail(PKV_ERR_INVALID_ARG,
                          "pkv_sched_run: suffix must be >= 0 and out_len in 1..max_out");
     }
     for (int32_t s = 1; s < S_; ++s)
-      for (int64_t t = 0; t < count_[s]; ++t) prefix_[base_[s] + t] = kv_len(s - 1, t / fanout_[s - 1]);
+      for (int64_t t = 0; t < count_[s]; ++t) {
+        prefix_[base_[s] + t] = kv_len(s - 1, t / fanout_[s - 1]);
+        if (prefix_[base_[s] + t] > INT32_MAX / 4)
+          return pkv::fail(PKV_ERR_INVALID_ARG, "pkv_sched_run: a task's prefix is too long");
+      }
+    if (max_kv_len() > INT32_MAX / 2)
+      return pkv::fail(PKV_ERR_INVALID_ARG, "pkv_sched_run: a task's sequence is too long");
     for (int32_t s = 0; s < S_; ++s) {
       int64_t mb = 0;
       for (int64_t t = 0; t < count_[s]; ++t)

@@ -98,6 +98,11 @@ def test_bad_configurations_are_refused(lib):
         with pytest.raises(lib.PkvError) as e:
             lib.pkv_sched_run(lib.sched_config(**kw), *args)
         assert e.value.status == lib.PKV_ERR_INVALID_ARG
+    huge = [np.full(len(a), 1 << 30) for a in d["suffix"]]  # lengths past the int32 range
+    with pytest.raises(lib.PkvError) as e:
+        lib.pkv_sched_run(lib.sched_config(0, 800, max_out=64), d["fanout"], huge,
+                          d["out_len"], d["filtered"])
+    assert e.value.status == lib.PKV_ERR_INVALID_ARG
     bad = dict(d)
     bad["suffix"] = [d["suffix"][0], d["suffix"][1][:-1]]
     with pytest.raises(Exception):
