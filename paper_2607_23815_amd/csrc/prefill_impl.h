@@ -78,49 +78,81 @@ struct PrefillSmem {
 constexpr float kRescaleThreshold = 8.0f;
 constexpr float kRescaleLimit = 256.0f;  // 2^kRescaleThreshold
 
-// The body of one prefill workgroup; `wg` is its index in the launch's work list (the
-// workgroup index of a prefill-only launch, a remapped one in a mixed launch).
+// ---- staging: direct global -> LDS 16-byte loads. Wave w stages block w % 4 of every
+// tile, sharing it with the other kWaves / 4 - 1 waves of that block: its load k fills LDS
+// units 64 (part * WLOADS + k) + lane of that block's slab (with four waves, the whole 4 KB
+// slab at head_dim 128 in four loads). The bank swizzle is applied on the global side: LDS K
+// unit c*16 + t holds global unit c*16 + swap23(t), LDS V unit 2d + t holds global unit
+// 2d + (t ^ ((d >> 3) & 1)); with these, the 16 lanes the LDS serves per cycle read 16
+// distinct 16-byte bank groups. ----
 template <int D>
-__device__ __forceinline__ void prefill_body(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
-                    const uint16_t* __restrict__ v_cache, const int32_t* __restrict__ block_tables,
-                    int32_t max_blocks, const int32_t* __restrict__ cached_lens,
-                    const int32_t* __restrict__ cu_new_lens, int32_t num_seqs, int32_t hq,
-                    int32_t hkv, int32_t num_blocks, int32_t qtiles, float scale_log2,
-                    uint16_t* __restrict__ out, float* __restrict__ lse, const unsigned wg) {
+struct Staging {
+  static constexpr int SLAB = D * kBlockSize;          // elements per block slab
+  static constexpr int UNITS = SLAB / 8;               // 16-byte units per block slab
+  static constexpr int WLOADS = UNITS / 64 / kSlabWaves;  // loads per wave per block slab
+  int slab, part;  // the block of a tile this wave stages; its share of it
+  // Per-lane element offsets of load 0 within a block slab; load k reads 512 k elements
+  // further on (the swizzles act within 64-unit groups), so two registers serve every load.
+  int kofs, vofs;
+  __device__ __forceinline__ Staging(int wave, int lane) : slab(wave & 3), part(wave >> 2) {
+    const int pos = part * WLOADS * 64 + lane;
+    const int c = pos >> 4;
+    kofs = (c * 16 + swap23(pos & 15)) * 8;
+    const int d = pos >> 1;
+    vofs = (2 * d + ((pos & 1) ^ ((d >> 3) & 1))) * 8;
+  }
+  template <int K>
+  __device__ __forceinline__ void issue_load(const uint16_t* src, uint16_t* dst, int ofs) const {
+    lds_load16(src, SLAB * 2, (ofs + K * 512) * 2, dst + slab * SLAB + (part * WLOADS + K) * 512);
+    if constexpr (K + 1 < WLOADS) issue_load<K + 1>(src, dst, ofs);
+  }
+  // This wave's share of block `blk` (kv head `kvh`) into the tile buffer `dst`, with offsets
+  // `ofs` (kofs or vofs). One slab = one buffer resource (base = the slab, 4 KB,
+  // bounds-checked by the hardware).
+  __device__ __forceinline__ void issue(const uint16_t* cache, uint16_t* dst, int ofs, int blk,
+                                        int hkv, int kvh) const {
+    issue_load<0>(cache + ((size_t)blk * hkv + kvh) * SLAB, dst, ofs);
+  }
+};
+
+// Q as the B operand of S^T = K Q^T: lane (lc, hh) of wave `wave` holds column
+// qt * kCols + 32 wave + lc, dims 16 kk + 8 hh .. +7. A lane past the last column reads a
+// valid row (token n - 1); the caller zeroes it before use.
+template <int D>
+__device__ __forceinline__ void load_q(const uint16_t* __restrict__ q, int hq, int hkv, int kvh,
+                                       int qt, int row0, int n, int wave, int lane,
+                                       bf16x8 (&qf)[D / 16]) {
+  const int g = hq / hkv;
+  const int gcol = qt * kCols + wave * 32 + (lane & 31);
+  const int j = gcol < n * g ? gcol / g : n - 1;
+  const int head = kvh * g + gcol % g;
+  const uint16_t* qrow = q + ((size_t)(row0 + j) * hq + head) * D + (lane >> 5) * 8;
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) qf[kk] = as_bf16x8(ld16(qrow + kk * 16));
+}
+
+// One work item: query tile qt (columns qt * kCols ..) of the (sequence i, kv head kvh)
+// group, whose cached prefix is p tokens and whose n new tokens start at row row0 of q and
+// out. t_first and t_lane are entry 0 and entry `lane` of the sequence's block-table row
+// (-1 past the row).
+template <int D>
+__device__ __forceinline__ void prefill_item(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
+    const uint16_t* __restrict__ v_cache, const int32_t* __restrict__ block_tables,
+    int32_t max_blocks, int32_t hq, int32_t hkv, int32_t num_blocks, float scale_log2,
+    uint16_t* __restrict__ out, float* __restrict__ lse, const int i, const int kvh,
+    const int qt, const int p, const int row0, const int n, const int32_t t_first,
+    const int32_t t_lane, PrefillSmem<D>& sm) {
   constexpr int SLAB = D * kBlockSize;
   constexpr int UNITS = SLAB / 8;        // 16-byte units per block slab
   constexpr int LPT = 4 * UNITS / kThreads;  // 16-byte units per thread per tile (K or V)
   constexpr int KK = D / 16;             // k-steps of the score product
   constexpr int DB = D / 32;             // 32-dim blocks of the value product
-  __shared__ __align__(16) PrefillSmem<D> sm;
 
-  // XCD-aware mapping: workgroup id b runs on XCD b % 8 (a mixed launch passes a `wg` with
-  // the same residue mod 8 as its workgroup id). The unit that must stay on one XCD
-  // is a (sequence, kv head) group -- its query tiles read the same K/V and share that XCD's
-  // L2 when they run together -- so groups are dealt to XCDs round-robin (group index mod 8)
-  // and each XCD walks its groups in order, query tiles longest first. With 8 kv heads every
-  // XCD receives one kv head of every sequence: equal work per XCD, whatever the lengths.
-  const int xcd = wg & 7;
-  const int pos = wg >> 3;                 // position in this XCD's list
-  const int group = (pos / qtiles) * 8 + xcd;      // (sequence, kv head) group index
-  const int qt = qtiles - 1 - pos % qtiles;        // longest (last) query tile first
-  if (group >= num_seqs * hkv) return;
-  const int kvh = group % hkv;
-  const int i = group / hkv;
-
-  // The first table chunk (entry `lane` of the sequence's row, and entry 0) is fetched
-  // before the lengths: its address depends on the sequence only, so the two loads overlap.
   const int32_t* table = block_tables + (size_t)i * max_blocks;
-  const int32_t t_first = table[0];
-  const int32_t t_lane = (int)(threadIdx.x & 63) < max_blocks ? table[threadIdx.x & 63] : -1;
-
   const int g = hq / hkv;
-  const int p = cached_lens[i];
-  const int row0 = cu_new_lens[i];
-  const int n = cu_new_lens[i + 1] - row0;
   const int ncols = n * g;
   const int col0 = qt * kCols;
-  if (col0 >= ncols) return;
   const int len = p + n;
 
   const int tid = threadIdx.x;
@@ -134,6 +166,7 @@ __device__ __forceinline__ void prefill_body(const uint16_t* __restrict__ q, con
   const int j = col_ok ? gcol / g : n - 1;
   const int head = kvh * g + gcol % g;
   const int lim = p + j;  // last key this column sees
+  const int lim_h = lim - 8 * hh;  // the same, less the lane's key offset within a block
 
   const int jmax = min(n - 1, (col0 + kCols - 1) / g);
   const int nkeys = p + jmax + 1;
@@ -142,7 +175,6 @@ __device__ __forceinline__ void prefill_body(const uint16_t* __restrict__ q, con
   const int wj_lo = min(wcol0 / g, n - 1);         // earliest token among the wave's columns
   const bool wave_live = wcol0 < ncols;            // the wave has at least one real column
 
-  bf16x8 qf[KK];  // Q fragments, loaded in the prologue
   f32x16 o[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db)
@@ -150,30 +182,14 @@ __device__ __forceinline__ void prefill_body(const uint16_t* __restrict__ q, con
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
   float m = -INFINITY;
   float lpart = 0.f;
+  bf16x8 qf[KK];  // Q fragments, loaded in the prologue
 
-  const size_t head_off = (size_t)kvh * SLAB;
   // stand-in for blocks past the sequence: its first block (len >= 1, so it owns one)
   const int32_t blk_first = (t_first >= 0 && t_first < num_blocks) ? t_first : 0;
+  const Staging<D> st(wave, lane);
+  constexpr int WLOADS = Staging<D>::WLOADS;
+  const int slab = st.slab;
 
-  // ---- staging: direct global -> LDS 16-byte loads. Wave w stages block w % 4 of every
-  // tile, sharing it with the other kWaves / 4 - 1 waves of that block: its load k fills LDS
-  // units 64 (part * WLOADS + k) + lane of that block's slab (with four waves, the whole
-  // 4 KB slab at head_dim 128 in four loads). The bank swizzle is applied on the global side: LDS K unit
-  // c*16 + t holds global unit c*16 + swap23(t), LDS V unit 2d + t holds global unit
-  // 2d + (t ^ ((d >> 3) & 1)); with these, the 16 lanes the LDS serves per cycle read 16
-  // distinct 16-byte bank groups. ----
-  constexpr int WLOADS = UNITS / 64 / kSlabWaves;  // loads per wave per block slab
-  const int slab = wave & 3;                       // the block of the tile this wave stages
-  const int part = wave >> 2;                      // which WLOADS loads of that slab
-  int kofs[WLOADS], vofs[WLOADS];        // per-lane element offsets within a block slab
-#pragma unroll
-  for (int k = 0; k < WLOADS; ++k) {
-    const int pos = (part * WLOADS + k) * 64 + lane;
-    const int c = pos >> 4;
-    kofs[k] = (c * 16 + swap23(pos & 15)) * 8;
-    const int d = pos >> 1;
-    vofs[k] = (2 * d + ((pos & 1) ^ ((d >> 3) & 1))) * 8;
-  }
   // Block-table entries through a per-wave register table: lane l of a chunk holds entry
   // 64 c + l, already checked (entries past the sequence, past the table or out of the pool
   // are replaced by the sequence's first block: finite data, masked or zeroed before use).
@@ -201,17 +217,11 @@ __device__ __forceinline__ void prefill_body(const uint16_t* __restrict__ q, con
     return __builtin_amdgcn_readlane(chunk, e & 63);
   };
   // One slab = one buffer resource (base = the slab, 4 KB, bounds-checked by the hardware).
-  auto issue = [&](const uint16_t* cache, uint16_t* dst, const int (&ofs)[WLOADS], int blk) {
-    const uint16_t* src = cache + (size_t)blk * hkv * SLAB + head_off;
-#pragma unroll
-    for (int k = 0; k < WLOADS; ++k)
-      lds_load16(src, SLAB * 2, ofs[k] * 2, dst + slab * SLAB + (part * WLOADS + k) * 512);
-  };
   auto issue_k = [&](int kt, int buf) {
-    issue(k_cache, sm.k[buf], kofs, block_of(kchunk, kchunk_id, kt));
+    st.issue(k_cache, sm.k[buf], st.kofs, block_of(kchunk, kchunk_id, kt), hkv, kvh);
   };
   auto issue_v = [&](int kt, int buf) {
-    issue(v_cache, sm.v[buf], vofs, block_of(vchunk, vchunk_id, kt));
+    st.issue(v_cache, sm.v[buf], st.vofs, block_of(vchunk, vchunk_id, kt), hkv, kvh);
   };
 
   // lane-constant LDS read offsets (elements)
@@ -239,13 +249,16 @@ __device__ __forceinline__ void prefill_body(const uint16_t* __restrict__ q, con
 
   // register r of half-tile beta holds the score of key
   // key0 + 32 beta + 16 (r/8) + 8 hh + 4 ((r/4) % 2) + r % 4
+  // (compared as a compile-time offset against lim - key0 - 8 hh, so no per-register key
+  // positions are kept live)
   auto mask_tile = [&](int key0, f32x16 (&sc)[2]) {
+    const int d = lim_h - key0;
 #pragma unroll
     for (int beta = 0; beta < 2; ++beta)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int key = key0 + 32 * beta + 16 * (r >> 3) + 8 * hh + 4 * ((r >> 2) & 1) + (r & 3);
-        sc[beta][r] = key <= lim ? sc[beta][r] : -INFINITY;
+        const int c = 32 * beta + 16 * (r >> 3) + 4 * ((r >> 2) & 1) + (r & 3);
+        sc[beta][r] = c <= d ? sc[beta][r] : -INFINITY;
       }
   };
 
@@ -363,22 +376,16 @@ __device__ __forceinline__ void prefill_body(const uint16_t* __restrict__ q, con
 
   // prologue: K(0), K(1) and V(0) (every buffer is free; their blocks are entries 0..7 of
   // the first chunk), then Q, all under one wait; scores of tile 0
-  issue(k_cache, sm.k[0], kofs, __builtin_amdgcn_readlane(kchunk, slab));
-  if (ntiles > 1) issue(k_cache, sm.k[1], kofs, __builtin_amdgcn_readlane(kchunk, 4 + slab));
-  issue(v_cache, sm.v[0], vofs, __builtin_amdgcn_readlane(kchunk, slab));
-  // Q as the B operand of S^T = K Q^T: lane holds Q[column lc][16 kk + 8 hh .. +7]. A lane
-  // past the last column reads a valid row (token n - 1) and keeps zeros, so the loads are
-  // unconditional and the wait above counts them exactly.
-  {
-    const uint16_t* qrow = q + ((size_t)(row0 + j) * hq + head) * D + hh * 8;
-    u32x4 qv[KK];
+  st.issue(k_cache, sm.k[0], st.kofs, __builtin_amdgcn_readlane(kchunk, slab), hkv, kvh);
+  if (ntiles > 1)
+    st.issue(k_cache, sm.k[1], st.kofs, __builtin_amdgcn_readlane(kchunk, 4 + slab), hkv, kvh);
+  st.issue(v_cache, sm.v[0], st.vofs, __builtin_amdgcn_readlane(kchunk, slab), hkv, kvh);
+  // Q fragments; a lane past the last column computes with zeros
+  load_q<D>(q, hq, hkv, kvh, qt, row0, n, wave, lane, qf);
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) qv[kk] = ld16(qrow + kk * 16);
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      const u32x4 zero = {0u, 0u, 0u, 0u};
-      qf[kk] = as_bf16x8(col_ok ? qv[kk] : zero);
-    }
+  for (int kk = 0; kk < KK; ++kk) {
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    qf[kk] = col_ok ? qf[kk] : as_bf16x8(zero);
   }
   wait_vmem();
   __syncthreads();
@@ -455,6 +462,42 @@ __device__ __forceinline__ void prefill_body(const uint16_t* __restrict__ q, con
       st8(orow + db * 32 + 8 * a + 4 * hh, w);
     }
   if (lse != nullptr && hh == 0) lse[(size_t)(row0 + j) * hq + head] = (m + log2f(l)) * kLn2;
+}
+
+// The body of one prefill workgroup of a one-item-per-workgroup launch (the mixed launch);
+// `wg` is its index in the launch's work list.
+template <int D>
+__device__ __forceinline__ void prefill_body(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
+                    const uint16_t* __restrict__ v_cache, const int32_t* __restrict__ block_tables,
+                    int32_t max_blocks, const int32_t* __restrict__ cached_lens,
+                    const int32_t* __restrict__ cu_new_lens, int32_t num_seqs, int32_t hq,
+                    int32_t hkv, int32_t num_blocks, int32_t qtiles, float scale_log2,
+                    uint16_t* __restrict__ out, float* __restrict__ lse, const unsigned wg) {
+  __shared__ __align__(16) PrefillSmem<D> sm;
+  // XCD-aware mapping: workgroup id b runs on XCD b % 8 (a mixed launch passes a `wg` with
+  // the same residue mod 8 as its workgroup id). The unit that must stay on one XCD
+  // is a (sequence, kv head) group -- its query tiles read the same K/V and share that XCD's
+  // L2 when they run together -- so groups are dealt to XCDs round-robin (group index mod 8)
+  // and each XCD walks its groups in order, query tiles longest first. With 8 kv heads every
+  // XCD receives one kv head of every sequence: equal work per XCD, whatever the lengths.
+  const int xcd = wg & 7;
+  const int pos = wg >> 3;                 // position in this XCD's list
+  const int group = (pos / qtiles) * 8 + xcd;      // (sequence, kv head) group index
+  const int qt = qtiles - 1 - pos % qtiles;        // longest (last) query tile first
+  if (group >= num_seqs * hkv) return;
+  const int kvh = group % hkv;
+  const int i = group / hkv;
+  // The first table chunk (entry `lane` of the sequence's row, and entry 0) is fetched
+  // before the lengths: its address depends on the sequence only, so the two loads overlap.
+  const int32_t* table = block_tables + (size_t)i * max_blocks;
+  const int32_t t_first = table[0];
+  const int32_t t_lane = (int)(threadIdx.x & 63) < max_blocks ? table[threadIdx.x & 63] : -1;
+  const int p = cached_lens[i];
+  const int row0 = cu_new_lens[i];
+  const int n = cu_new_lens[i + 1] - row0;
+  if (qt * kCols >= n * (hq / hkv)) return;
+  prefill_item<D>(q, k_cache, v_cache, block_tables, max_blocks, hq, hkv, num_blocks, scale_log2,
+                  out, lse, i, kvh, qt, p, row0, n, t_first, t_lane, sm);
 }
 
 // The work list of a prefill batch: query tiles per (sequence, kv head) group, and the
