@@ -78,6 +78,11 @@ EDGES = [
     ("gqa4_d128", 32, 8, 128, [0, 1, 16, 255, 256, 257], [64, 1, 17, 33, 128, 3]),
     ("gqa8_d128", 64, 8, 128, [0, 31, 512, 47, 2, 700], [5, 16, 100, 130, 256, 1]),
     ("gqa8_d64", 16, 2, 64, [0, 200, 3, 64, 1, 9], [300, 7, 16, 1, 64, 40]),
+    # one kv head for 16 query heads (8 tokens per query tile); a prefix of 132 blocks, past
+    # the 64-entry block-table chunk each wave keeps in registers
+    ("mqa16_d128", 16, 1, 128, [0, 100, 1000, 3, 16, 2100], [1, 40, 9, 300, 16, 2]),
+    # sequences with no new tokens between others: no output rows, nothing launched for them
+    ("empty_rows", 32, 8, 128, [5, 0, 300, 17, 1024, 0], [0, 3, 0, 50, 0, 1]),
 ]
 
 
@@ -88,6 +93,27 @@ def test_prefill_edge_shapes(gpu_lib, edge):
     spec = _edge_spec(name, 100 + EDGES.index(edge), hq, hkv, d, len(prefixes))
     case = W.make_case(spec, prefix_override=[prefixes], new_override=[news])
     check(name, case, run_prefill(gpu_lib, case), oracle_prefill(case))
+
+
+def test_prefill_host_maxima_are_upper_bounds(gpu_lib):
+    """max_new_len and max_total_len only size the launch: larger values give the same bits
+    (the extra query tiles are empty)."""
+    import torch
+    say("[prefill] inflated host maxima")
+    case = W.make_case(W.LLAMA3_8B_PREFILL.scaled(prefill=4))
+    b = case.batches[0]
+    pk, pv = dev_pools(case)
+    db = DevBatch(b)
+    gpu_lib.pkv_kv_append(pk, pv, db.k_new, db.v_new, db.tables, db.cached, db.cu, db.max_new)
+    outs = []
+    wide = int(b.block_tables.shape[1]) * case.bs  # the most the table can describe
+    for mn, mt in ((db.max_new, db.max_total), (3 * db.max_new, wide)):
+        out = torch.empty((b.total_new, case.hq, case.d), dtype=torch.bfloat16, device="cuda")
+        gpu_lib.pkv_prefill_attention(pk, pv, db.q, db.tables, db.cached, db.cu, mn, mt,
+                                      scale_for(case.d), out)
+        torch.cuda.synchronize()
+        outs.append(to_host_bits(out))
+    assert np.array_equal(outs[0], outs[1])
 
 
 def test_prefill_is_deterministic_and_placement_invariant(gpu_lib):
