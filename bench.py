@@ -560,6 +560,31 @@ def pipelines(args, lib, torch):
     return out
 
 
+def achievable_peaks(torch):
+    """Context for the rooflines, measured on the same GPU in the same run: a library bf16
+    GEMM (torch.matmul, 8192^3, hipBLASLt) and a plain 1 GiB device copy (read + write).
+    These are what stock library code reaches here, not the datasheet peaks the fractions
+    use."""
+    stream = torch.cuda.current_stream()
+    n = 8192
+    a = torch.randn(n, n, device="cuda").to(torch.bfloat16)
+    b = torch.randn(n, n, device="cuda").to(torch.bfloat16)
+    c = torch.empty(n, n, device="cuda", dtype=torch.bfloat16)
+    _, _, per = time_events(torch, stream, [lambda: torch.matmul(a, b, out=c)], 10, 2)
+    gemm = 2.0 * n ** 3 / per[0] / 1e12
+    del a, b, c
+    m = 1 << 30
+    x = torch.empty(m, dtype=torch.uint8, device="cuda")
+    y = torch.empty_like(x)
+    x.fill_(1)
+    _, _, per = time_events(torch, stream, [lambda: y.copy_(x)], 10, 2)
+    copy = 2 * m / per[0] / 1e9
+    del x, y
+    torch.cuda.empty_cache()
+    return {"gemm_bf16_8192_TFLOP_s": gemm, "gemm_frac_of_peak": gemm / PEAK_BF16_TFLOPS,
+            "copy_1GiB_GB_s": copy, "copy_frac_of_peak": copy / PEAK_HBM_GBS}
+
+
 def profile_copy(args, torch):
     """A plain device copy of known size (1 GiB read + 1 GiB written per launch): the
     reference that scales the L2<->HBM byte counters to bytes."""
@@ -683,6 +708,7 @@ def main():
         log("[bench] secondary workloads ...")
         res["secondary"] = secondary(args, lib, torch)
         res["secondary"]["reuse_vs_recompute"] = reuse_vs_recompute(args, lib, torch)
+        res["secondary"]["achievable_peaks"] = achievable_peaks(torch)
         log("[bench] pipelines under the scheduler ...")
         res["secondary"]["pipelines"] = pipelines(args, lib, torch)
         log("[bench] secondary done")
