@@ -569,11 +569,11 @@ def achievable_peaks(torch):
     n = 8192
     a = torch.randn(n, n, device="cuda").to(torch.bfloat16)
     b = torch.randn(n, n, device="cuda").to(torch.bfloat16)
-    c = torch.empty(n, n, device="cuda", dtype=torch.bfloat16)
     bt = b.t()  # [K][N] view of a row-major [N][K] operand
-    _, _, per = time_events(torch, stream, [lambda: torch.matmul(a, bt, out=c)], 10, 2)
-    gemm = 2.0 * n ** 3 / per[0] / 1e12
-    del a, b, c
+    # best of two timed sets: the first one also settles the library's kernel choice
+    gemm = max(2.0 * n ** 3 / time_events(torch, stream, [lambda: torch.matmul(a, bt)], 10, 2)[2][0]
+               / 1e12 for _ in range(2))
+    del a, b, bt
     m = 1 << 30
     x = torch.empty(m, dtype=torch.uint8, device="cuda")
     y = torch.empty_like(x)
