@@ -478,12 +478,18 @@ __device__ __forceinline__ void prefill_body(const uint16_t* __restrict__ q, con
   // the same residue mod 8 as its workgroup id). The unit that must stay on one XCD
   // is a (sequence, kv head) group -- its query tiles read the same K/V and share that XCD's
   // L2 when they run together -- so groups are dealt to XCDs round-robin (group index mod 8)
-  // and each XCD walks its groups in order, query tiles longest first. With 8 kv heads every
-  // XCD receives one kv head of every sequence: equal work per XCD, whatever the lengths.
+  // and each XCD walks its groups in order. With 8 kv heads every XCD receives one kv head of
+  // every sequence: equal work per XCD, whatever the lengths.
+  // Within a group the query tiles go longest (last) first, rotated by the group's place in
+  // the XCD's list: an XCD hands its workgroups to its shader engines in a fixed rotation,
+  // and without the rotation slot s of every group -- and with it the low tiles, the ones
+  // every sequence has -- would always land on the same engine, which then fills first and
+  // stalls the rotation while the others have free slots.
   const int xcd = wg & 7;
   const int pos = wg >> 3;                 // position in this XCD's list
-  const int group = (pos / qtiles) * 8 + xcd;      // (sequence, kv head) group index
-  const int qt = qtiles - 1 - pos % qtiles;        // longest (last) query tile first
+  const int gpos = pos / qtiles;           // the group's place in this XCD's list
+  const int group = gpos * 8 + xcd;        // (sequence, kv head) group index
+  const int qt = qtiles - 1 - (pos % qtiles + gpos) % qtiles;
   if (group >= num_seqs * hkv) return;
   const int kvh = group % hkv;
   const int i = group / hkv;
