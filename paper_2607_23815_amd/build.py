@@ -3,7 +3,9 @@
     python -m paper_2607_23815_amd.build
 
 Packed fp32 instructions are disabled for all device code (-packed-fp32-ops): the kernels use
-plain fp32 arithmetic only."""
+plain fp32 arithmetic only. The machine scheduler runs its instruction-level-parallelism
+strategy (-amdgpu-sched-strategy=max-ilp): the prefill's matrix-core/softmax block gains about
+1% from it, the HBM-bound kernels are unchanged, and every kernel's output is bit-identical."""
 import os
 import shutil
 import subprocess
@@ -30,6 +32,7 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     cmd = [hipcc(), "-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-shared",
            "-fvisibility=hidden", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           "-mllvm", "-amdgpu-sched-strategy=max-ilp",
            "-Wall", "-Wno-unused-function", "-I", os.path.join(ROOT, "include"),
            "-o", tmp] + [os.path.join(CSRC, s) for s in SOURCES]
     if verbose:
