@@ -449,19 +449,48 @@ __device__ __forceinline__ void prefill_item(
   }
 
   const float l = lpart + swap_halves(lpart);
-  if (!col_ok) return;
-  const float inv = 1.f / l;
-  uint16_t* orow = out + ((size_t)(row0 + j) * hq + head) * D;
+  if (!wave_live) return;
+  // The wave's 32 output rows go out through LDS as whole rows: a lane holds 8-byte pieces
+  // of one row (column), so storing them directly would put 32 rows into every store
+  // instruction; written to LDS first (the K buffers, free since the last step's barrier:
+  // 32 rows x D per wave), each 16-byte store below covers 64 / (D / 8) complete rows.
+  // 16-byte unit u of row r sits at unit u ^ (r % (D / 8)), so that both the 8-byte writes
+  // (32 rows at once) and the 16-byte reads (whole rows) spread over all LDS banks.
+  constexpr int CH = D / 8;    // 16-byte units per row
+  constexpr int RPI = 64 / CH; // rows per store instruction
+  uint16_t* tile = &sm.k[0][0] + wave * 32 * D;
+  // the lane index afresh (an opaque copy), so that no value derived from it for this block
+  // is computed ahead of the step loop and kept live through it
+  int ln;
+  asm volatile("v_and_b32 %0, 63, %1" : "=v"(ln) : "v"((int)threadIdx.x));
+  const int lcl = ln & 31, hhl = ln >> 5;
+  {
+    const float inv = 1.f / l;  // columns past the end: any value, never stored
 #pragma unroll
-  for (int db = 0; db < DB; ++db)
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
-      // registers 4a .. 4a+3 hold dims 32 db + 8 a + 4 hh + 0..3
-      u32x2 w = {pack_bf16x2(o[db][4 * a + 0] * inv, o[db][4 * a + 1] * inv),
-                 pack_bf16x2(o[db][4 * a + 2] * inv, o[db][4 * a + 3] * inv)};
-      st8(orow + db * 32 + 8 * a + 4 * hh, w);
+      for (int a = 0; a < 4; ++a) {
+        // registers 4a .. 4a+3 hold dims 32 db + 8 a + 4 hh + 0..3
+        u32x2 w = {pack_bf16x2(o[db][4 * a + 0] * inv, o[db][4 * a + 1] * inv),
+                   pack_bf16x2(o[db][4 * a + 2] * inv, o[db][4 * a + 3] * inv)};
+        const int u = (4 * db + a) ^ (lcl % CH);
+        st8(tile + lcl * D + u * 8 + 4 * hhl, w);
+      }
+  }
+#pragma unroll
+  for (int k = 0; k < 32 / RPI; ++k) {
+    const int r = k * RPI + ln / CH;  // the row (wave column) this lane stores a unit of
+    const int u = ln % CH;
+    const u32x4 v = ld16(tile + r * D + ((u ^ (r % CH)) * 8));
+    const int gc = wcol0 + r;
+    if (gc < ncols) {
+      const int jr = gc / g;
+      st16(out + ((size_t)(row0 + jr) * hq + kvh * g + gc % g) * D + u * 8, v);
     }
-  if (lse != nullptr && hh == 0) lse[(size_t)(row0 + j) * hq + head] = (m + log2f(l)) * kLn2;
+  }
+  const int gcl = wcol0 + lcl;  // this lane's column, recomputed like the lane index
+  if (lse != nullptr && hhl == 0 && gcl < ncols)
+    lse[(size_t)(row0 + gcl / g) * hq + kvh * g + gcl % g] = (m + log2f(l)) * kLn2;
 }
 
 // The body of one prefill workgroup of a one-item-per-workgroup launch (the mixed launch);
