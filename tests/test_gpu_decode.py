@@ -58,7 +58,8 @@ CONTEXTS = [0, 1, 14, 15, 16, 17, 30, 31, 32, 33, 63, 64, 127, 255, 256, 257, 51
             2047, 2048, 4095]
 
 
-@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (64, 8, 128), (4, 2, 64), (16, 1, 128)])
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (64, 8, 128), (4, 2, 64), (16, 1, 128),
+                                      (28, 4, 128)])
 def test_decode_split_and_block_boundaries(gpu_lib, hq, hkv, d):
     say(f"[decode] boundaries hq={hq} hkv={hkv} d={d}")
     spec = W.WorkloadSpec(f"decode_edges_{hq}_{hkv}_{d}", 140 + hq + d, hq, hkv, d,

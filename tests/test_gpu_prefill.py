@@ -83,6 +83,11 @@ EDGES = [
     ("mqa16_d128", 16, 1, 128, [0, 100, 1000, 3, 16, 2100], [1, 40, 9, 300, 16, 2]),
     # sequences with no new tokens between others: no output rows, nothing launched for them
     ("empty_rows", 32, 8, 128, [5, 0, 300, 17, 1024, 0], [0, 3, 0, 50, 0, 1]),
+    # a group of 7 query heads (28/4): tokens straddle the 32-column waves and the output
+    # rows of one store instruction belong to different tokens
+    ("gqa7_d128", 28, 4, 128, [0, 77, 16, 500, 1, 260], [1, 45, 64, 9, 130, 33]),
+    # a group of 32 (one token per wave), head dim 64 (8 output rows per store instruction)
+    ("mqa32_d64", 32, 1, 64, [3, 0, 129, 640, 48, 2], [17, 70, 1, 5, 40, 128]),
 ]
 
 
