@@ -25,9 +25,12 @@
 //      32-key half-tile is loaded with key sigma(m), sigma swapping bits 2 and 3 of the key
 //      index; then the 8 keys a lane contributes to each value-product step are 8
 //      consecutive slots, i.e. one 16-byte chunk of the dim-major V slab.
+//   5. The normalised output rows leave through LDS (the K buffers, free after the last
+//      step), so that each 16-byte store covers whole rows.
 // Masking is by selection (scores to -inf), applied only to tiles that reach past some
-// column's last visible key; V slots past the sequence end are zeroed while staging, so stale
-// bits (NaN included) never meet a zero weight inside the matrix core.
+// column's last visible key; V slots past the sequence end are zeroed in LDS before the last
+// tile's value product, so stale bits (NaN included) never meet a zero weight inside the
+// matrix core.
 #pragma once
 
 #include <math.h>
