@@ -221,8 +221,9 @@ typedef struct {
  * tuple's cached prefix with its own suffix. For each sequence i < num_seqs and each new
  * token j < N_i = cu_new_lens[i+1] - cu_new_lens[i], row cu_new_lens[i] + j of k_new / v_new
  * (bf16 [total_new][num_kv_heads][head_dim], row-major) is copied bit-exactly into logical
- * position cached_lens[i] + j of sequence i. No other byte of the pool is written (the V
- * slots of a partially covered 16-byte chunk are stored one by one). block_tables: int32 [num_seqs][max_blocks]; cached_lens: int32 [num_seqs];
+ * position cached_lens[i] + j of sequence i. No other byte of the pool is modified (a
+ * partially covered 16-byte V chunk is read and written back unchanged outside the new
+ * slots). block_tables: int32 [num_seqs][max_blocks]; cached_lens: int32 [num_seqs];
  * cu_new_lens: int32 [num_seqs + 1], cu_new_lens[0] = 0, non-decreasing,
  * cu_new_lens[num_seqs] = total_new. max_new_len (host) >= every N_i sizes the grid. The
  * target blocks must be private to the sequence (the allocator guarantees this). */

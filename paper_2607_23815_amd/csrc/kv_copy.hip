@@ -8,10 +8,9 @@
 //   V: the pool slab is [head_dim][16 slots] (dim-major), a transpose of the token rows. The
 //      rows are staged in LDS with coalesced 16-byte loads, then each thread assembles the
 //      8 slots of one dim-row half and stores them as one 16-byte chunk. A half that is only
-//      partly covered by new tokens (the first block continuing a cached prefix, the last
-//      block, a decode token) gets 2-byte stores of its new slots only, so slots outside the
-//      new range keep their bits without being read (reading and writing the half back cost
-//      the Llama-3-8B suffix append 11%: the workgroup waited on the read).
+//      partly covered by new tokens (the first block continuing a cached prefix, or the last
+//      block) is read, merged and written back, so slots outside the new range keep their
+//      bits; no other sequence can write the block (new tokens only go to private blocks).
 // Whole 16-byte chunks are written with non-temporal stores (the appended rows are not read
 // again by this launch): 64% -> 69% of HBM peak on the Llama-3-8B suffix append.
 #include "device_utils.h"
@@ -78,18 +77,19 @@ __global__ __launch_bounds__(256) void kv_append_kernel(
     const int a = max(lo, s0), e = min(lo + 8, s1);
     if (a >= e) continue;
     uint16_t* dst = v_cache + slab + (size_t)d * kBlockSize + lo;
+    uint16_t vals[8];
     if (a == lo && e == lo + 8) {
-      uint16_t vals[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) vals[k] = tile[(lo + k) * ROW + d];
-      u32x4 packed;
-      __builtin_memcpy(&packed, vals, 16);
-      st16_nt(dst, packed);
     } else {
-      // a half only partly new (a decode token, the ends of a suffix): 2-byte stores of the
-      // new slots, so the half's other slots need not be read and written back
-      for (int k = a; k < e; ++k) dst[k - lo] = tile[k * ROW + d];
+      const u32x4 old = ld16(dst);
+      __builtin_memcpy(vals, &old, 16);
+      for (int k = a; k < e; ++k) vals[k - lo] = tile[k * ROW + d];
     }
+    u32x4 packed;
+    __builtin_memcpy(&packed, vals, 16);
+    if (a == lo && e == lo + 8) st16_nt(dst, packed);
+    else st16(dst, packed);  // a merged half: the block may be read again soon
   }
 }
 
