@@ -167,7 +167,6 @@ __device__ __forceinline__ void prefill_item(
   const int gcol = col0 + wave * 32 + lc;
   const bool col_ok = gcol < ncols;
   const int j = col_ok ? gcol / g : n - 1;
-  const int head = kvh * g + gcol % g;
   const int lim = p + j;  // last key this column sees
   const int lim_h = lim - 8 * hh;  // the same, less the lane's key offset within a block
 
@@ -190,7 +189,6 @@ __device__ __forceinline__ void prefill_item(
   // stand-in for blocks past the sequence: its first block (len >= 1, so it owns one)
   const int32_t blk_first = (t_first >= 0 && t_first < num_blocks) ? t_first : 0;
   const Staging<D> st(wave, lane);
-  constexpr int WLOADS = Staging<D>::WLOADS;
   const int slab = st.slab;
 
   // Block-table entries through a per-wave register table: lane l of a chunk holds entry
