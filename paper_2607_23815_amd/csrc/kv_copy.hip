@@ -97,6 +97,60 @@ __global__ __launch_bounds__(256) void kv_append_kernel(
   }
 }
 
+// The append of one token per sequence (a decode step; max_new_len == 1): one wave per
+// (sequence, kv head). The token's K row goes to its slot as 16-byte chunks (16 lanes at head
+// dim 128); each lane owns D/64 V dims and rewrites the 16-byte half-row holding the slot.
+// Every load (the new row, the old halves) is issued before any store, so the wave waits
+// once; the general kernel would spend two 256-thread workgroups (one empty) on each.
+template <int D>
+__global__ __launch_bounds__(64) void kv_append_token_kernel(
+    const uint16_t* __restrict__ k_new, const uint16_t* __restrict__ v_new,
+    uint16_t* __restrict__ k_cache, uint16_t* __restrict__ v_cache,
+    const int32_t* __restrict__ block_tables, int32_t max_blocks,
+    const int32_t* __restrict__ cached_lens, const int32_t* __restrict__ cu_new_lens,
+    int32_t hkv, int32_t num_blocks) {
+  constexpr int NCH = D / 8;           // 16-byte chunks per token row
+  constexpr int SLAB = D * kBlockSize;  // elements per (block, head) slab
+  constexpr int DPL = D / 64;          // V dims per lane
+  static_assert(DPL == 1 || DPL == 2, "head dim 64 or 128");
+  const int i = blockIdx.y;
+  const int h = blockIdx.x;
+  const int row = cu_new_lens[i];
+  if (cu_new_lens[i + 1] - row <= 0) return;
+  const int p = cached_lens[i];
+  const int b = p / kBlockSize;
+  if (b >= max_blocks) return;
+  const int blk = block_tables[(size_t)i * max_blocks + b];
+  if (blk < 0 || blk >= num_blocks) return;
+  const int s = p % kBlockSize;
+  const size_t slab = ((size_t)blk * hkv + h) * SLAB;
+  const int lane = threadIdx.x;
+  const uint16_t* krow = k_new + ((size_t)row * hkv + h) * D;
+  const uint16_t* vrow = v_new + ((size_t)row * hkv + h) * D;
+  // loads: this lane's K chunk, its V dims and the old halves holding slot s of those dims
+  u32x4 kval = {0u, 0u, 0u, 0u};
+  if (lane < NCH) kval = ld16(krow + lane * 8);
+  uint16_t vnew[DPL];
+  u32x4 vold[DPL];
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) {
+    const int d = lane * DPL + e;
+    vnew[e] = vrow[d];
+    vold[e] = ld16(v_cache + slab + (size_t)d * kBlockSize + (s & 8));
+  }
+  if (lane < NCH) st16(k_cache + slab + (size_t)(lane * kBlockSize + s) * 8, kval);
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) {
+    const int d = lane * DPL + e;
+    uint16_t vals[8];
+    __builtin_memcpy(vals, &vold[e], 16);
+    vals[s & 7] = vnew[e];
+    u32x4 packed;
+    __builtin_memcpy(&packed, vals, 16);
+    st16(v_cache + slab + (size_t)d * kBlockSize + (s & 8), packed);
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(256) void gather_kv_kernel(
     const uint16_t* __restrict__ k_cache, const uint16_t* __restrict__ v_cache,
@@ -142,6 +196,18 @@ hipError_t launch_kv_append(const KvView& kv, const uint16_t* k_new, const uint1
                             const int32_t* block_tables, int32_t max_blocks,
                             const int32_t* cached_lens, const int32_t* cu_new_lens,
                             int32_t num_seqs, int32_t max_new_len, hipStream_t stream) {
+  if (max_new_len == 1) {  // one token per sequence (a decode step)
+    const dim3 tgrid(kv.hkv, num_seqs);
+    if (kv.head_dim == 128)
+      hipLaunchKernelGGL(kv_append_token_kernel<128>, tgrid, dim3(64), 0, stream, k_new, v_new,
+                         kv.k, kv.v, block_tables, max_blocks, cached_lens, cu_new_lens, kv.hkv,
+                         kv.num_blocks);
+    else
+      hipLaunchKernelGGL(kv_append_token_kernel<64>, tgrid, dim3(64), 0, stream, k_new, v_new,
+                         kv.k, kv.v, block_tables, max_blocks, cached_lens, cu_new_lens, kv.hkv,
+                         kv.num_blocks);
+    return hipGetLastError();
+  }
   // new tokens of one sequence touch at most ceil(max_new_len / 16) + 1 blocks
   dim3 grid((max_new_len + kBlockSize - 1) / kBlockSize + 1, kv.hkv, num_seqs);
   if (kv.head_dim == 128)

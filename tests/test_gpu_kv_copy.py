@@ -93,3 +93,29 @@ def test_append_head_dim_64_many_heads(gpu_lib):
                                     b.cu_new_lens, b.k_new, b.v_new, 16)
     assert np.array_equal(to_host_bits(pk), ref_k)
     assert np.array_equal(to_host_bits(pv), ref_v)
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (8, 2, 64)])
+def test_append_one_token_per_sequence(gpu_lib, hq, hkv, d):
+    """A decode step's append (max_new_len == 1, its own launch shape): every slot position in
+    a block, sequences with no token, bit-exact over the whole pool (stale NaN canaries
+    included)."""
+    import torch
+    lib = gpu_lib
+    say(f"[append] one token per sequence hq={hq} hkv={hkv} d={d}")
+    prefixes = [0, 1, 7, 8, 9, 15, 16, 17, 31, 100, 255, 256, 5, 40]
+    news = [1] * 12 + [0, 1]
+    spec = W.WorkloadSpec(f"append_token_{d}", 95 + d, hq, hkv, d,
+                          (W.BatchSpec("prefill", len(prefixes), W.Dist.const(1),
+                                       W.Dist.const(1)),), ("scale", 1.5))
+    case = W.make_case(spec, prefix_override=[prefixes], new_override=[news])
+    b = case.batches[0]
+    pk, pv = dev_pools(case)
+    db = DevBatch(b)
+    assert db.max_new == 1
+    lib.pkv_kv_append(pk, pv, db.k_new, db.v_new, db.tables, db.cached, db.cu, db.max_new)
+    torch.cuda.synchronize()
+    ref_k, ref_v = oracle.kv_append(case.pool_k, case.pool_v, b.block_tables, b.prefix_lens,
+                                    b.cu_new_lens, b.k_new, b.v_new, 16)
+    assert np.array_equal(to_host_bits(pk), ref_k)
+    assert np.array_equal(to_host_bits(pv), ref_v)
