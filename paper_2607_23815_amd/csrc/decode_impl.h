@@ -135,19 +135,19 @@ __device__ __forceinline__ void decode_body(
   const int32_t* table = block_tables + (size_t)i * max_blocks;
   const int b_first = k0 / kBlockSize;
   const int nblk = (k1 - k0 + kBlockSize - 1) / kBlockSize;
-  auto load_chunk = [&](int c) -> int {
+  // (the load and the check are separate steps, so that the first two chunks' loads are both
+  // in flight before either is checked)
+  auto raw_chunk = [&](int c) -> int {
     const int r = 64 * c + lane;
     const int b = b_first + r;
-    int e = 0;
-    if (r < nblk && b < max_blocks) {
-      e = table[b];
-      if (e < 0 || e >= num_blocks) e = 0;
-    }
-    return e;
+    return (r < nblk && b < max_blocks) ? table[b] : 0;
   };
+  auto checked = [&](int e) -> int { return (e < 0 || e >= num_blocks) ? 0 : e; };
+  auto load_chunk = [&](int c) -> int { return checked(raw_chunk(c)); };
   int chunk = 0;
-  int tab = load_chunk(0);
-  int tab_next = load_chunk(1);
+  const int raw0 = raw_chunk(0), raw1 = raw_chunk(1);
+  int tab = checked(raw0);
+  int tab_next = checked(raw1);
   const size_t head_off = (size_t)kvh * SLAB;
   // block b (0 <= b < 128) counted from the start of the current chunk
   auto block_off = [&](int b) -> size_t {
