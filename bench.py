@@ -41,7 +41,7 @@ def log(msg):
 
 
 # ---------------------------------------------------------------------------------------
-# algorithmic work ("Measurement")
+# algorithmic work: the figures the measured times are divided by
 # ---------------------------------------------------------------------------------------
 def prefill_flops(prefix, new, hq, d):
     p = prefix.astype(np.float64)
@@ -684,7 +684,8 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this path needs no collective and runs one "
-              "process on one MI355X (see DESIGN.md for how it would shard).", file=sys.stderr)
+              "process on one MI355X; tuples are independent, so more GPUs would each run "
+              "their own share of them.", file=sys.stderr)
         sys.exit(2)
     import torch
     if not torch.cuda.is_available():

@@ -6,7 +6,7 @@ operator's prompt `[S | C(t) | I_op]` reuses the cached KV of `[S | C(t)]` left 
 operator and prefills only `I_op`, after which decode runs over the same cache. The paper's
 datasets are not used; every tensor is a seeded N(0,1) draw rounded to bf16.
 
-Readings where the workload text leaves a choice open (each is listed in the design doc):
+Readings where the workload text leaves a choice open:
   * uniform[a, b] is a discrete uniform over the integers a..b, both ends included, drawn
     independently per sequence;
   * a decode "context length" C is the number of tokens already cached; the step appends one
