@@ -506,7 +506,7 @@ def pipelines(args, lib, torch):
     policy, every engine step's append, block copies and prefill/decode attention on the GPU
     (one attention layer, Llama-3-8B heads). The KV pool holds about 64 first-stage tuples'
     prefixes, so the table does not fit: blocking execution loses its prefixes to the cache
-    (Section 3's cliff) while the memory-aware schedule keeps them. gpu_ms is the summed GPU
+    (Section 2.2's cliff) while the memory-aware schedule keeps them. gpu_ms is the summed GPU
     time of the steps; the host schedules between steps (wall_ms)."""
     from workloads.pipelines import PIPELINES, make_pipeline
     hq, hkv, d, src_rows = 32, 8, 128, 8192

@@ -25,7 +25,7 @@ Semantics (each from the paper, with the readings this project takes):
     through copy-on-write.
   * Eviction: when a reservation finds too few free blocks, resident entries are dropped in
     policy order until enough blocks are free -- least recently used first by default, most
-    recently used first as the alternative Section 3 weighs. Every entry not protected by a
+    recently used first as the alternative Section 2.2 weighs. Every entry not protected by a
     pin is a candidate; dropping it releases its references, and only blocks that no sequence
     or other entry still holds return to the free list (a running sequence keeps what it
     shares). Recency is a logical clock advanced by publish and by each hit. Reading: ties

@@ -1,11 +1,11 @@
 """Plain model of the pipelined semantic-operator scheduler (oracle; test infrastructure only).
 
 What it follows:
-  * Section 5.2 (query execution): a pipeline of stages; a task runs one stage's operator on one
+  * Section 5.1 (executing query plans): a pipeline of stages; a task runs one stage's operator on one
     tuple; a surviving task of a non-final stage is joined (Cartesian product) with the next
     stage's right-side table, creating dependent child tasks that reuse the task's cached
     prefix; a final-stage task's result is output; a filtered task ends its branch.
-  * Algorithm 1 (Section 5.4): Schedule iterates Launch (per stage, in stage order, admit the
+  * Algorithm 1 (Section 5.3): Schedule iterates Launch (per stage, in stage order, admit the
     head of the waiting queue while the memory manager admits it), then Complete for every
     finished task (retry with a larger bound; enqueue children and track the dependency; output;
     release memory), then Rebalance (saturated stages other than the first give Delta to the
@@ -21,8 +21,9 @@ What it follows:
     relies on the pool's eviction order.
   * Section 5.3's baselines: sequential depth-first (one task at a time, deepest stage first),
     parallel depth-first (the initial budgets, never rebalanced), parallel breadth-first (a
-    static large first-stage budget), and the blocking execution of Section 3 (each stage runs
-    to completion before the next starts; prefixes are left to the LRU cache).
+    static large first-stage budget), and blocking execution, the operator-at-a-time
+    materialisation of Section 2.2 that Section 7.4 ablates (each stage runs to completion
+    before the next starts; prefixes are left to the LRU cache).
 
 Readings where the paper is silent (the library implements the same ones):
   * Memory is counted in 16-token KV blocks of the pool. A task's charge is the blocks it adds:

@@ -37,7 +37,8 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(
   const int lane = threadIdx.x & 63;
   if (item >= (int64_t)num_seqs * hq) return;
   const int i = (int)(item / hq);
-  const int len = seq_lens[i];
+  // the partial kernel's cut of an over-long length (at most max_splits splits)
+  const int len = min(seq_lens[i], max_splits * split_keys);
   const int nsplit = (len + split_keys - 1) / split_keys;
   if (nsplit <= 1) return;  // written directly by the partial kernel
   const size_t base = (size_t)item * max_splits;

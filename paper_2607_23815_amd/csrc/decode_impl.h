@@ -111,11 +111,17 @@ __device__ __forceinline__ void decode_body(
   const int rem = (int)(item % per_seq);
   const int kvh = rem / max_splits;
   const int sp = rem % max_splits;
-  const int len = seq_lens[i];
-  const int nsplit = (len + split_keys - 1) / split_keys;
+  // A length above the host's max_seq_len breaks the caller's contract; it is cut to the
+  // splits the launch planned (the merge cuts it the same way), and keys past the table are
+  // not attended, so such a call computes over fewer keys but never leaves its workspace.
+  // With max_seq_len <= max_blocks * 16 (checked on the host) every planned split starts
+  // inside the table, so no split is empty.
+  const int len = min(seq_lens[i], max_splits * split_keys);
+  const int nsplit = (len + split_keys - 1) / split_keys;  // 0 for a length < 1: no output
   if (sp >= nsplit) return;
   const int k0 = sp * split_keys;
-  const int k1 = min(len, k0 + split_keys);
+  int k1 = min(len, k0 + split_keys);
+  if ((k1 - 1) / kBlockSize >= max_blocks) k1 = max_blocks * kBlockSize;  // (no overflow)
   const bool col_ok = col < g;
   const int h = kvh * g + col;
 

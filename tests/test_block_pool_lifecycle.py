@@ -2,10 +2,10 @@
 recovery, copy-on-write; oracle/block_pool.py) against what the paper states and what the
 definitions fix, on the CPU:
 
-  * Section 3's cache-miss experiment: two operators over the same table with a prefix cache
+  * Section 2.2's cache-miss experiment: two operators over the same table with a prefix cache
     of C tuples. Under LRU the second operator hits every tuple while the table fits and none
     once it does not (the cliff the paper measures); MRU keeps a constant number of hits
-    however large the table grows, a bounded gain as Section 3 argues. The expected counts are worked
+    however large the table grows, a bounded gain as Section 2.2 argues. The expected counts are worked
     out by hand in the test, not by the model.
   * Section 6: a pinned prefix is never evicted until it is unpinned; virtual pinning leaves
     eviction to the LRU order; waiting requests with none running is a deadlock whose
@@ -66,7 +66,7 @@ def prefill_tuple(m, key, tokens):
 
 
 def two_operator_hits(table, capacity_tuples, policy, blocks_per_tuple=3):
-    """Section 3's experiment: operator 1 prefills every tuple, then operator 2 reuses each
+    """Section 2.2's experiment: operator 1 prefills every tuple, then operator 2 reuses each
     tuple's prefix (a hit) or recomputes it (a miss)."""
     m = BlockPoolModel(capacity_tuples * blocks_per_tuple, BS)
     m.set_eviction(policy)

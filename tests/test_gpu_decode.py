@@ -114,3 +114,53 @@ def test_decode_equals_single_token_prefill(gpu_lib):
     case2.batches[0].kind = "prefill"
     p_out, _ = run_prefill(gpu_lib, case2)
     compare("decode vs prefill", bf16_to_f64(d_out), bf16_to_f64(p_out))
+
+
+def _oracle_first_keys(case, b, seq_lens_cut, scale):
+    """Decode of each sequence's query over its first seq_lens_cut[i] cached keys (no append)."""
+    g = case.hq // case.hkv
+    out = np.zeros((b.n_seqs, case.hq, case.d))
+    lse = np.zeros((b.n_seqs, case.hq))
+    for i in range(b.n_seqs):
+        L = int(seq_lens_cut[i])
+        kc, vc = oracle.gather_seq(case.pool_k, case.pool_v, b.block_tables[i], L, case.bs)
+        kf, vf = oracle.bf16_bits_to_f64(kc), oracle.bf16_bits_to_f64(vc)
+        qi = oracle.bf16_bits_to_f64(b.q[i])
+        for h in range(case.hq):
+            o, l = oracle.softmax_attention(qi[h][None], kf[:, h // g], vf[:, h // g], [L], scale)
+            out[i, h], lse[i, h] = o[0], l[0]
+    return out, lse
+
+
+@pytest.mark.parametrize("hq,hkv,d,ctx,max_len,cut", [
+    # one split per sequence planned (grid of 2048 waves): the over-long row is cut to 4096
+    (16, 8, 64, [4200] + [20] * 255, 4096, 4096),
+    # five 64-key splits planned: the over-long row is cut to 5 x 64 keys
+    (32, 8, 128, [1000, 50, 60, 70], 300, 320),
+])
+def test_decode_over_long_length_is_cut_to_the_planned_splits(gpu_lib, hq, hkv, d, ctx, max_len,
+                                                              cut):
+    """A sequence longer than the host's max_seq_len (a broken caller contract) is cut to the
+    splits the launch planned: the call stays inside its workspace (no split beyond the
+    planned ones, no partial result without a workspace slot) and attends over that many
+    keys; every other row is unaffected."""
+    import torch
+    say(f"[decode] over-long length hq={hq} hkv={hkv} d={d} B={len(ctx)} max_seq_len={max_len}")
+    spec = W.WorkloadSpec(f"decode_overlong_{hq}_{d}", 160 + d, hq, hkv, d,
+                          (W.BatchSpec("decode", len(ctx), W.Dist.const(1),
+                                       W.Dist.const(1)),), ("scale", 1.25))
+    case = W.make_case(spec, prefix_override=[ctx])
+    b = case.batches[0]
+    pk, pv = dev_pools(case)
+    db = DevBatch(b)
+    lens = np.asarray(ctx, dtype=np.int32)   # every key cached: no append in this test
+    out = torch.empty((b.n_seqs, hq, d), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((b.n_seqs, hq), dtype=torch.float32, device="cuda")
+    ws = gpu_lib.alloc_workspace(gpu_lib.pkv_decode_workspace_bytes(b.n_seqs, hq, hkv, d,
+                                                                    max_len))
+    assert b.block_tables.shape[1] * 16 >= max_len
+    gpu_lib.pkv_decode_attention(pk, pv, db.q, db.tables, i32(lens), max_len, scale_for(d), out,
+                                 lse=lse, workspace=ws)
+    torch.cuda.synchronize()
+    ref = _oracle_first_keys(case, b, np.minimum(lens, cut), scale_for(d))
+    check(spec.name, (to_host_bits(out), lse.cpu().numpy().astype(np.float64)), ref)

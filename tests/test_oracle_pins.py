@@ -292,6 +292,43 @@ def test_pi7_append_writes_exactly_the_new_slots():
     assert ck.shape[0] == sum(prefixes) + T
 
 
+def test_pi7_gather_kv_concatenates_sequences_in_order():
+    """Pi7 for the multi-sequence gather: sequences of distinct lengths (0, one token, ends
+    mid-block, whole blocks, several blocks) are placed into scattered blocks element by
+    element by the test-side fixture; row r of the gathered K/V must be token r - start_i of
+    sequence i, where start_i is the sum of the earlier lengths -- checked row by row against
+    the contiguous tensors the pools were built from. Any other order, a dropped or repeated
+    sequence, or a transposed chunk layout fails it."""
+    rng = np.random.default_rng(23)
+    hkv, d = 3, 64
+    lens = [7, 0, 16, 1, 41, 33, 32]
+    nblk = [-(-n // BS) for n in lens]
+    num_blocks = sum(nblk) + 5
+    perm = rng.permutation(num_blocks)
+    tables = np.full((len(lens), max(nblk)), -1, np.int32)
+    pk, pv = empty_pools(num_blocks, hkv, d, BS)
+    cur = 0
+    src_k, src_v = [], []
+    for i, n in enumerate(lens):
+        tables[i, :nblk[i]] = perm[cur:cur + nblk[i]]
+        cur += nblk[i]
+        kk, vv = rand_bf16(rng, (n, hkv, d)), rand_bf16(rng, (n, hkv, d))
+        place(pk, pv, tables[i], kk, vv, BS)
+        src_k.append(kk)
+        src_v.append(vv)
+    ck, cv = oracle.gather_kv(pk, pv, tables, lens, BS)
+    assert ck.shape == (sum(lens), hkv, d) and cv.shape == ck.shape
+    r = 0
+    for i, n in enumerate(lens):
+        for t in range(n):
+            assert np.array_equal(ck[r], src_k[i][t]), (i, t)
+            assert np.array_equal(cv[r], src_v[i][t]), (i, t)
+            r += 1
+    assert r == ck.shape[0]
+    # no NaN canary (an unwritten slot) is gathered
+    assert not np.any(ck == 0x7FC0) and not np.any(cv == 0x7FC0)
+
+
 def test_pi8_kv_footprint_matches_paper():
     """Pi8: 2 * layers * kv_heads * head_dim * 2 bytes reproduces Section 2.2's 112 KB/token,
     84 MB per 750-token tuple and ~70 tuples in ~6 GB."""

@@ -9,7 +9,7 @@ definitions fix and against values worked out by hand:
     the tasks' output lengths (Section 5.3);
   * explicit pinning never loses a prefix its children need (Section 6): no cache misses;
     blocking execution over a table larger than the cache misses every prefix, and over a small
-    table misses none (Section 3's cliff);
+    table misses none (Section 2.2's cliff);
   * a request that hits its bound is retried with a doubled bound (Section 6), worked by hand;
   * the token bound is the nearest-rank 99th percentile of observed ratios, worked by hand;
   * rebalancing: the first transfers of a small two-stage run, worked by hand; budgets always
