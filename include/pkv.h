@@ -124,7 +124,7 @@ pkv_status pkv_seq_len(const pkv_pool* pool, int64_t seq, int32_t* len);
  *
  * Eviction: when a reservation (pkv_seq_reserve / pkv_seq_reserve_cow) finds too few free
  * blocks, entries are dropped in policy order until enough are free, all-or-nothing like
- * the reservation itself. Policy (Section 3 weighs both): least recently used first
+ * the reservation itself. Policy (Section 2.2 weighs both): least recently used first
  * (default) or most recently used first, by a logical clock that each publish and each hit
  * advances. Dropping an entry releases its references only: a block returns to the back of
  * the free list when its last holder (sequence or entry) lets go, so a running sequence
@@ -273,6 +273,24 @@ pkv_status pkv_decode_attention(const pkv_paged_kv* kv, const void* q, int32_t n
 size_t pkv_decode_workspace_bytes(int32_t num_seqs, int32_t num_q_heads, int32_t num_kv_heads,
                                   int32_t head_dim, int32_t max_seq_len);
 
+/* Allocation-free decode, for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc. The same computation
+ * as pkv_decode_attention (same kernels, bit-identical results) with the same arguments but
+ * no workspace: the library uses a fixed device array of PKV_DECODE_NOALLOC_MAX_BYTES bytes per
+ * GPU instead, loaded with the library's code object and held until the process ends. Calls
+ * whose pkv_decode_workspace_bytes exceeds that size return PKV_ERR_INVALID_ARG before any
+ * launch. The call itself allocates nothing (no hipMalloc, no library allocation); its first
+ * call on a device looks the array's address up once. Every call on a GPU shares that GPU's
+ * array, so calls that overlap on one GPU (different streams, or different host threads)
+ * race and must be serialised by the caller. Nothing in the array needs to start at zero:
+ * each call writes every word it later reads. */
+#define PKV_DECODE_NOALLOC_MAX_BYTES (((size_t)32) << 20)
+pkv_status pkv_decode_attention_noalloc(const pkv_paged_kv* kv, const void* q,
+                                        int32_t num_q_heads, const int32_t* block_tables,
+                                        int32_t max_blocks, const int32_t* seq_lens,
+                                        int32_t num_seqs, int32_t max_seq_len, float scale,
+                                        void* out, float* lse, void* stream);
+
 /* Block copy (the device half of copy-on-write): for each k < num_pairs, the K and V of
  * every kv head in block pairs[2k] are copied bit-exactly into block pairs[2k+1]. pairs:
  * int32 device memory [num_pairs][2], e.g. the pairs pkv_seq_reserve_cow returned; every
@@ -345,7 +363,8 @@ pkv_status pkv_gather_kv(const pkv_paged_kv* kv, const int32_t* block_tables,
  * stages but the last, which takes the rest) and never rebalances; BREADTH_FIRST gives the
  * first stage breadth_share of the pool statically; SEQUENTIAL runs one task at a time, the
  * deepest ready stage first; BLOCKING runs each stage to completion before the next and leaves
- * prefixes to the cache's eviction order (the materialising execution of Section 3).
+ * prefixes to the cache's eviction order (the materialising execution of Section 2.2, ablated in
+ * Section 7.4).
  * --------------------------------------------------------------------------------------- */
 #define PKV_MAX_STAGES 8
 enum { PKV_SCHED_ADAPTIVE = 0, PKV_SCHED_DEPTH_FIRST = 1, PKV_SCHED_BREADTH_FIRST = 2,

@@ -96,12 +96,13 @@ pkv_status check_prefill(const KvView& view, const char* fn, const void* q, int3
   return ok();
 }
 
-// Argument checks of a decode batch (decode and mixed calls).
+// Argument checks of a decode batch (decode and mixed calls). With scratch set the call
+// brings no workspace: the fixed scratch array must hold what it needs.
 pkv_status check_decode(const KvView& view, const char* fn, const void* q, int32_t num_q_heads,
                         const int32_t* block_tables, int32_t max_blocks,
                         const int32_t* seq_lens, int32_t num_seqs, int32_t max_seq_len,
                         float scale, const void* out, const void* workspace,
-                        size_t workspace_bytes, bool* empty) {
+                        size_t workspace_bytes, bool* empty, bool scratch = false) {
   const std::string f(fn);
   *empty = false;
   if (num_q_heads <= 0 || num_q_heads % view.hkv != 0 || num_q_heads / view.hkv > 16)
@@ -125,6 +126,15 @@ pkv_status check_decode(const KvView& view, const char* fn, const void* q, int32
   if (!(scale > 0.f)) return fail(PKV_ERR_INVALID_ARG, f + ": scale <= 0");
   const size_t need = decode_workspace_bytes(num_seqs, num_q_heads, view.hkv, view.head_dim,
                                              max_seq_len);
+  if (scratch) {
+    if (need > kDecodeScratchBytes)
+      return fail(PKV_ERR_INVALID_ARG,
+                  f + ": the call needs " + std::to_string(need) +
+                      " bytes of workspace, above the fixed scratch of " +
+                      std::to_string(kDecodeScratchBytes) +
+                      " bytes (pkv_decode_attention takes a caller-owned workspace)");
+    return ok();
+  }
   if (need > 0 && (workspace == nullptr || workspace_bytes < need || !aligned16(workspace)))
     return fail(PKV_ERR_INVALID_ARG,
                 f + ": workspace missing, too small or not 16-byte aligned "
@@ -225,6 +235,31 @@ pkv_status pkv_decode_attention(const pkv_paged_kv* kv, const void* q, int32_t n
   return launched(launch_decode(view, static_cast<const uint16_t*>(q), num_q_heads,
                                 block_tables, max_blocks, seq_lens, num_seqs, max_seq_len, scale,
                                 static_cast<uint16_t*>(out), lse, workspace,
+                                static_cast<hipStream_t>(stream)),
+                  fn);
+}
+
+pkv_status pkv_decode_attention_noalloc(const pkv_paged_kv* kv, const void* q,
+                                        int32_t num_q_heads, const int32_t* block_tables,
+                                        int32_t max_blocks, const int32_t* seq_lens,
+                                        int32_t num_seqs, int32_t max_seq_len, float scale,
+                                        void* out, float* lse, void* stream) {
+  const char* fn = "pkv_decode_attention_noalloc";
+  static_assert(PKV_DECODE_NOALLOC_MAX_BYTES == kDecodeScratchBytes,
+                "the header's limit is the scratch array's size");
+  KvView view;
+  pkv_status st = check_kv(kv, fn, &view);
+  if (st != PKV_OK) return st;
+  bool empty = false;
+  st = check_decode(view, fn, q, num_q_heads, block_tables, max_blocks, seq_lens, num_seqs,
+                    max_seq_len, scale, out, nullptr, 0, &empty, /*scratch=*/true);
+  if (st != PKV_OK || empty) return st;
+  void* ws = nullptr;
+  const hipError_t err = decode_scratch(&ws);
+  if (err != hipSuccess) return launched(err, fn);
+  return launched(launch_decode(view, static_cast<const uint16_t*>(q), num_q_heads,
+                                block_tables, max_blocks, seq_lens, num_seqs, max_seq_len, scale,
+                                static_cast<uint16_t*>(out), lse, ws,
                                 static_cast<hipStream_t>(stream)),
                   fn);
 }

@@ -2,6 +2,8 @@
 // items, and the merge of split partial results). The work-item body is in decode_impl.h.
 #include <math.h>
 
+#include <mutex>
+
 #include "decode_impl.h"
 #include "launch.h"
 
@@ -109,7 +111,33 @@ size_t order_bytes(int32_t num_seqs) {
   return ((size_t)num_seqs * sizeof(int32_t) + 255) / 256 * 256;
 }
 
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
 }  // namespace
+
+// The allocation-free decode's workspace: one array per GPU, loaded with the code object and
+// held until the process ends. Its device address comes from hipGetSymbolAddress, taken once
+// per device with that device current; the array's name in host code is a host-side stand-in
+// and never goes to a kernel or a copy.
+static __device__ __align__(256) unsigned char scratch[kDecodeScratchBytes];
+
+hipError_t decode_scratch(void** ptr) {
+  int dev = 0;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) return err;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (err != hipSuccess) return err;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
+}
 
 int32_t decode_split_keys(int32_t num_seqs, int32_t hkv, int32_t max_seq_len) {
   // Longest split first (every split pays a prologue of dependent table and first KV loads

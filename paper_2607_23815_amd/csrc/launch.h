@@ -62,6 +62,11 @@ hipError_t launch_decode(const KvView& kv, const uint16_t* q, int32_t hq,
                          float scale, uint16_t* out, float* lse, void* workspace,
                          hipStream_t stream);
 
+// The allocation-free decode's workspace (a file-scope device array of kDecodeScratchBytes):
+// its address on the current device, looked up on the first call per device.
+constexpr size_t kDecodeScratchBytes = size_t(32) << 20;
+hipError_t decode_scratch(void** ptr);
+
 // Mixed launch: a prefill batch (arguments as launch_prefill) and a decode batch (d_*, as
 // launch_decode, with its workspace) in one fused kernel between the decode's ordering
 // kernel and its merge. Both batches must be non-empty.

@@ -122,6 +122,9 @@ _SIGS = {
                                        c_int32, c_void_p, c_int32, c_int32, c_float, c_void_p,
                                        c_void_p, c_void_p, c_size_t, c_void_p]),
     "pkv_decode_workspace_bytes": (c_size_t, [c_int32] * 5),
+    "pkv_decode_attention_noalloc": (c_int32, [ctypes.POINTER(PagedKV), c_void_p, c_int32,
+                                               c_void_p, c_int32, c_void_p, c_int32, c_int32,
+                                               c_float, c_void_p, c_void_p, c_void_p]),
     "pkv_mixed_attention": (c_int32, [ctypes.POINTER(PagedKV), c_int32, c_float, c_void_p,
                                       c_void_p, c_int32, c_void_p, c_void_p, c_int32, c_int32,
                                       c_int32, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
@@ -454,6 +457,24 @@ def pkv_decode_attention(k_cache, v_cache, q, block_tables, seq_lens, max_seq_le
         _dev_ptr(seq_lens, "seq_lens", torch.int32), b, int(max_seq_len), float(scale),
         _dev_ptr(out, "out", torch.bfloat16), _dev_ptr(lse, "lse", torch.float32),
         _dev_ptr(workspace, "workspace"), ws_bytes, _stream(stream)))
+
+
+PKV_DECODE_NOALLOC_MAX_BYTES = 32 << 20
+
+
+def pkv_decode_attention_noalloc(k_cache, v_cache, q, block_tables, seq_lens, max_seq_len: int,
+                                 scale: float, out, lse=None, stream=None) -> None:
+    """pkv_decode_attention without a workspace argument: the library's fixed per-GPU
+    scratch array serves instead (nothing is allocated here or in the library)."""
+    import torch
+    kv = paged_kv(k_cache, v_cache)
+    b, hq, d = q.shape
+    _check(_lib.pkv_decode_attention_noalloc(
+        ctypes.byref(kv), _dev_ptr(q, "q", torch.bfloat16), hq,
+        _dev_ptr(block_tables, "block_tables", torch.int32), int(block_tables.shape[1]),
+        _dev_ptr(seq_lens, "seq_lens", torch.int32), b, int(max_seq_len), float(scale),
+        _dev_ptr(out, "out", torch.bfloat16), _dev_ptr(lse, "lse", torch.float32),
+        _stream(stream)))
 
 
 def pkv_mixed_attention(k_cache, v_cache, scale: float,

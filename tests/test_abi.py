@@ -333,3 +333,23 @@ def test_decode_workspace_is_a_function_of_sizes(lib):
     assert lib.pkv_decode_workspace_bytes(4096, 32, 8, 128, 60) == 4096 * 4
     assert lib.pkv_decode_workspace_bytes(3, 32, 8, 128, 60) == 256
     assert lib.pkv_prefill_workspace_bytes(256, 40000, 32, 8, 128, 256, 1280) == 0
+
+
+def test_noalloc_decode_refuses_oversize_calls_on_the_host(lib):
+    """The allocation-free decode's fixed scratch holds PKV_DECODE_NOALLOC_MAX_BYTES; a call
+    needing more is refused before any launch (so no GPU is touched here), with the size in
+    the message; an empty call is a no-op."""
+    L = lib._lib
+    kv = lib.PagedKV(ctypes.c_void_p(0x1000), ctypes.c_void_p(0x2000), 1 << 20, 16, 8, 128)
+    fake = ctypes.c_void_p(0x3000)
+    need = lib.pkv_decode_workspace_bytes(4096, 64, 8, 128, 16384)
+    assert need > lib.PKV_DECODE_NOALLOC_MAX_BYTES
+    assert L.pkv_decode_attention_noalloc(ctypes.byref(kv), fake, 64, fake, 1024, fake, 4096,
+                                          16384, 0.1, fake, None, None) == lib.PKV_ERR_INVALID_ARG
+    msg = lib.pkv_last_error()
+    assert str(need) in msg and "scratch" in msg
+    # the other argument checks are those of pkv_decode_attention
+    assert L.pkv_decode_attention_noalloc(ctypes.byref(kv), fake, 34, fake, 4, fake, 1, 1, 0.1,
+                                          fake, None, None) == lib.PKV_ERR_UNSUPPORTED_SHAPE
+    assert L.pkv_decode_attention_noalloc(ctypes.byref(kv), None, 64, None, 0, None, 0, 0, 0.1,
+                                          None, None, None) == lib.PKV_OK
