@@ -1,21 +1,27 @@
 #!/usr/bin/env python3
 """Benchmark of the paged prefix-reuse attention hot path on one MI355X.
 
-One step = one downstream-operator pass over the Llama-3-8B-shaped prefix-reuse workload
-(256 tuples, 32 query / 8 kv heads, head_dim 128, cached prefix U[256,1024], new tokens
-U[64,256], 40k-block pool with random placement):
-    kv_append (the new tokens)  ->  prefill attention (new tokens over prefix + suffix)
-    kv_append (one decode token per tuple)  ->  decode attention (split-K + merge)
+One step = one serving step of a mixed pipelined batch on a 70B-shaped attention layer (64
+query / 8 kv heads, head_dim 128, block size 16), the largest configuration that fits one GPU:
+128 downstream-operator prefills (cached prefix U[512,2048], new tokens U[128,512]) and 384
+decodes (context U[256,4096]) on one pool with random block placement:
+    kv_append (the prefill suffixes) -> kv_append (one token per decoding sequence)
+    -> mixed attention (the prefill and decode batches fused in one launch)
 Block tables come from the library's allocator (checked equal to the generator's placement)
-and are resident in HBM with every input before the timed region starts.
+and every input is resident in HBM before the timed region starts. Each timed step is bracketed
+by HIP events on the stream the library launches on, and 768 MiB of an unrelated buffer are
+read between steps (outside the events) so that no step reads what the previous one left in
+the memory-side cache; figures are medians over the steps (p10 / p90 beside them).
 
-Prints ONE JSON line: value = tuples per second per attention layer for the whole step, plus
-the per-kernel figures, the roofline of the dominant kernel (prefill: bf16 matrix cores),
-the CPU oracle timed on a bounded sample of the same workload, and secondary workloads
-(paged decode, the mixed 70B-shaped batch, long documents with a shared prompt).
+Prints ONE JSON line: value = sequences (tuples) per second per attention layer for the
+whole step, per-kernel figures, the roofline of the dominant kernel (the fused launch: bf16
+matrix cores), the CPU oracle timed on a bounded sample of the same batch, and secondary
+workloads (the tiny case in microseconds, the Llama-3-8B prefix-reuse step, the 512-sequence
+paged decode, long documents with a shared prompt, reuse vs recompute, achievable peaks, the
+scheduler's pipelines). A compact per-workload summary goes to stderr at the end.
 
     python bench.py [--steps K] [--warmup W] [--no-secondary] [--no-cpu-baseline]
-    python bench.py --profile-kernel {prefill,decode,append} [--workload NAME] [--steps K]
+    python bench.py --profile-kernel {prefill,decode,append,mixed,copy} [--workload NAME]
         (launches only that kernel, for rocprofv3 kernel-trace and counter passes)
 """
 import argparse
@@ -62,6 +68,10 @@ def decode_bytes(seq_lens, hq, hkv, d):
     return float(kv + qo)
 
 
+def decode_flops(seq_lens, hq, d):
+    return float(4.0 * d * hq * np.sum(seq_lens.astype(np.float64)))
+
+
 def append_bytes(total_new, hkv, d):
     return float(total_new * hkv * d * 2 * 2 * 2)  # K and V, read + write
 
@@ -78,6 +88,7 @@ KERNEL_SOURCES = {
     "prefill": ("prefill.hip", "prefill_impl.h", "device_utils.h"),
     "decode": ("decode.hip", "decode_impl.h", "device_utils.h"),
     "append": ("kv_copy.hip", "device_utils.h"),
+    "mixed": ("mixed.hip", "prefill_impl.h", "decode_impl.h", "decode.hip", "device_utils.h"),
 }
 
 
@@ -178,20 +189,38 @@ class Workload:
 
 
 CLOCK_RAMP_S = 0.1
+FLUSH_BYTES = 768 << 20   # read between timed steps: three times the 256 MB MALL
 
 
-def time_events(torch, stream, fns, steps, warmup):
-    """Run the list of callables `steps` times after `warmup`, with an event before and
-    after each; returns (total seconds, per-callable mean seconds). Before the warmup, the
-    same callables run untimed for at least CLOCK_RAMP_S of wall time: on MI355X the shader
-    clock climbs from about 1.7 to about 2.05 GHz over the first ~30 ms of sustained load
-    (measured in-kernel), and a serving GPU is never cold."""
+class Flush:
+    """Reads FLUSH_BYTES of an unrelated buffer between timed steps (outside the events), so
+    that no step finds in the memory-side cache (MALL, 256 MB) or the L2s what the previous
+    one left there. A read leaves the caches holding clean lines: a write-based flush would
+    leave up to 256 MB of dirty lines whose write-back the next step would pay for."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.buf = torch.ones(FLUSH_BYTES // 4, dtype=torch.int32, device="cuda")
+
+    def __call__(self):
+        self.torch.sum(self.buf)
+
+
+def time_steps(torch, stream, fns, steps, warmup, flush=None):
+    """Run the callables `steps` times after `warmup` untimed runs, an event before and after
+    each; between steps, `flush` (outside the events). Before the warmup the same callables
+    run untimed for at least CLOCK_RAMP_S of wall time: on MI355X the shader clock climbs
+    from about 1.7 to about 2.05 GHz over the first ~30 ms of sustained load (measured
+    in-kernel), and a serving GPU is never cold. Returns (wall seconds per step including the
+    flushes, step seconds [steps], per-callable seconds [steps][len(fns)])."""
     t_ramp = time.perf_counter()
     while time.perf_counter() - t_ramp < CLOCK_RAMP_S:
         for f in fns:
             f()
         torch.cuda.synchronize()
     for _ in range(warmup):
+        if flush is not None:
+            flush()
         for f in fns:
             f()
     torch.cuda.synchronize()
@@ -199,16 +228,35 @@ def time_events(torch, stream, fns, steps, warmup):
           for _ in range(steps)]
     t0 = time.perf_counter()
     for s in range(steps):
+        if flush is not None:
+            flush()
         ev[s][0].record(stream)
         for k, f in enumerate(fns):
             f()
             ev[s][k + 1].record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    per = [float(np.mean([ev[s][k].elapsed_time(ev[s][k + 1]) for s in range(steps)])) / 1e3
-           for k in range(len(fns))]
-    gpu_total = float(np.mean([ev[s][0].elapsed_time(ev[s][-1]) for s in range(steps)])) / 1e3
-    return wall / steps, gpu_total, per
+    wall = (time.perf_counter() - t0) / steps
+    per = np.array([[ev[s][k].elapsed_time(ev[s][k + 1]) for k in range(len(fns))]
+                    for s in range(steps)]) / 1e3
+    step = np.array([ev[s][0].elapsed_time(ev[s][-1]) for s in range(steps)]) / 1e3
+    return wall, step, per
+
+
+def time_events(torch, stream, fns, steps, warmup, flush=None):
+    """time_steps reduced to medians: (wall s per step, step s, [per-callable s])."""
+    wall, step, per = time_steps(torch, stream, fns, steps, warmup, flush)
+    return wall, med(step), [med(per[:, k]) for k in range(len(fns))]
+
+
+def dist(x, scale=1e3):
+    """median / p10 / p90 of a sample (default: seconds -> ms)."""
+    x = np.asarray(x, dtype=np.float64) * scale
+    return {"median": float(np.median(x)), "p10": float(np.percentile(x, 10)),
+            "p90": float(np.percentile(x, 90))}
+
+
+def med(x):
+    return float(np.median(np.asarray(x, dtype=np.float64)))
 
 
 def frac(a, p):
@@ -216,93 +264,125 @@ def frac(a, p):
 
 
 # ---------------------------------------------------------------------------------------
-# primary: prefix-reuse prefill step (+ first decode step) on the Llama-3-8B layer
+# primary: the mixed 70B-shaped layer (the largest single-GPU configuration)
 # ---------------------------------------------------------------------------------------
-def primary(args, lib, torch):
-    import workloads as W
-    spec = W.LLAMA3_8B_PREFILL
-    wl = Workload(spec, lib, torch)
-    b, _ = wl.batches[0]
-    dv = wl.dev[0]
-    case = wl.case
-    stream = torch.cuda.current_stream()
-    T = b.total_new
-    out = torch.empty((T, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
-    lse = torch.empty((T, wl.hq), dtype=torch.float32, device="cuda")
-    dec = wl.decode_followup(0, lib, torch)
-    B = b.n_seqs
-    dout = torch.empty((B, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
-    dlse = torch.empty((B, wl.hq), dtype=torch.float32, device="cuda")
-    ws = lib.alloc_workspace(lib.pkv_decode_workspace_bytes(B, wl.hq, wl.hkv, wl.d,
-                                                            dec["max_len"]))
-    pk, pv = case.pool_k, case.pool_v
+PRIMARY = "mixed_70b_layer"
 
-    fns = [
-        lambda: lib.pkv_kv_append(pk, pv, b.k_new, b.v_new, dv["tables"], dv["cached"],
-                                  dv["cu"], dv["max_new"]),
-        lambda: lib.pkv_prefill_attention(pk, pv, b.q, dv["tables"], dv["cached"], dv["cu"],
-                                          dv["max_new"], dv["max_total"], wl.scale, out,
-                                          lse=lse),
-        lambda: lib.pkv_kv_append(pk, pv, dec["k"], dec["v"], dec["tables"], dec["ctx"],
-                                  dec["cu"], 1),
-        lambda: lib.pkv_decode_attention(pk, pv, dec["q"], dec["tables"], dec["seq_lens"],
-                                         dec["max_len"], wl.scale, dout, lse=dlse,
-                                         workspace=ws),
-    ]
-    step_wall, step_gpu, per = time_events(torch, stream, fns, args.steps, args.warmup)
-    t_app, t_pre, t_app1, t_dec = per
-    flops = prefill_flops(b.prefix_lens, b.new_lens, wl.hq, wl.d)
-    pbytes = prefill_bytes(b.prefix_lens, b.new_lens, wl.hq, wl.hkv, wl.d)
-    abytes = append_bytes(T, wl.hkv, wl.d)
-    dbytes = decode_bytes(dec["host_ctx"] + 1, wl.hq, wl.hkv, wl.d)
-    ms = step_wall * 1e3
+
+def primary(args, lib, torch, flush):
+    """One step = the serving step of a mixed pipelined batch on one 70B-shaped attention layer
+    (64 query / 8 kv heads, head_dim 128): 128 downstream-operator prefills (cached prefix
+    U[512,2048], new U[128,512]) and 384 decodes (context U[256,4096]) on one pool:
+        kv_append (the prefill suffixes) -> kv_append (one token per decoding sequence)
+        -> mixed attention (prefill and decode fused in one launch, then the split merge).
+    The same batch as separate prefill and decode launches is timed beside it."""
+    import workloads as W
+    from tests.gpu_util import i32
+    spec = W.BY_NAME[PRIMARY]
+    wl = Workload(spec, lib, torch)
+    (bp, _), (bd, _) = wl.batches
+    dp, dd = wl.dev
+    pk, pv = wl.case.pool_k, wl.case.pool_v
+    stream = torch.cuda.current_stream()
+    Tp = bp.total_new
+    op = torch.empty((Tp, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
+    od = torch.empty((bd.n_seqs, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
+    seq_lens = bd.prefix_lens + 1
+    sl = i32(seq_lens)
+    maxl = int(seq_lens.max())
+    ws = lib.alloc_workspace(lib.pkv_decode_workspace_bytes(bd.n_seqs, wl.hq, wl.hkv, wl.d,
+                                                            maxl))
+    app_p = lambda: lib.pkv_kv_append(pk, pv, bp.k_new, bp.v_new, dp["tables"], dp["cached"],
+                                      dp["cu"], dp["max_new"])
+    app_d = lambda: lib.pkv_kv_append(pk, pv, bd.k_new, bd.v_new, dd["tables"], dd["cached"],
+                                      dd["cu"], 1)
+    mixed = lambda: lib.pkv_mixed_attention(pk, pv, wl.scale, bp.q, dp["tables"], dp["cached"],
+                                            dp["cu"], dp["max_new"], dp["max_total"], op, bd.q,
+                                            dd["tables"], sl, maxl, od, workspace=ws)
+    pre = lambda: lib.pkv_prefill_attention(pk, pv, bp.q, dp["tables"], dp["cached"], dp["cu"],
+                                            dp["max_new"], dp["max_total"], wl.scale, op)
+    dec = lambda: lib.pkv_decode_attention(pk, pv, bd.q, dd["tables"], sl, maxl, wl.scale, od,
+                                           workspace=ws)
+    wall, step, per = time_steps(torch, stream, [app_p, app_d, mixed], args.steps, args.warmup,
+                                 flush)
+    _, step_s, per_s = time_steps(torch, stream, [app_p, app_d, pre, dec], args.steps,
+                                  args.warmup, flush)
+    B = bp.n_seqs + bd.n_seqs
+    pflops = prefill_flops(bp.prefix_lens, bp.new_lens, wl.hq, wl.d)
+    dflops = decode_flops(seq_lens, wl.hq, wl.d)
+    pbytes = prefill_bytes(bp.prefix_lens, bp.new_lens, wl.hq, wl.hkv, wl.d)
+    dbytes = decode_bytes(seq_lens, wl.hq, wl.hkv, wl.d)
+    abytes_p = append_bytes(Tp, wl.hkv, wl.d)
+    abytes_d = append_bytes(bd.n_seqs, wl.hkv, wl.d)
+    t_mixed = med(per[:, 2])
+    t_pre, t_dec = med(per_s[:, 2]), med(per_s[:, 3])
+    ideal_mixed = max((pflops + dflops) / (PEAK_BF16_TFLOPS * 1e12),
+                      (pbytes + dbytes) / (PEAK_HBM_GBS * 1e9))
     kernels = {
-        "kv_append": {"ms": t_app * 1e3, "tokens": T, "alg_bytes": abytes,
-                      "GB_s": abytes / t_app / 1e9, "frac_hbm": abytes / t_app / 1e9 / PEAK_HBM_GBS},
-        "prefill_attention": {"ms": t_pre * 1e3, "alg_flops": flops, "alg_bytes": pbytes,
-                              "TFLOP_s": flops / t_pre / 1e12,
-                              "frac_mfma": flops / t_pre / 1e12 / PEAK_BF16_TFLOPS},
-        "kv_append_decode_token": {"ms": t_app1 * 1e3, "tokens": B,
-                                   "alg_bytes": append_bytes(B, wl.hkv, wl.d),
-                                   "note": "launch-latency bound (4 MB); no roofline claim"},
-        "decode_attention": {"ms": t_dec * 1e3, "alg_bytes": dbytes,
-                             "GB_s": dbytes / t_dec / 1e9,
-                             "frac_hbm": dbytes / t_dec / 1e9 / PEAK_HBM_GBS},
+        "kv_append_suffixes": {"ms": dist(per[:, 0]), "tokens": Tp, "alg_bytes": abytes_p,
+                               "GB_s": abytes_p / med(per[:, 0]) / 1e9,
+                               "frac_hbm": abytes_p / med(per[:, 0]) / 1e9 / PEAK_HBM_GBS},
+        "kv_append_decode_tokens": {"ms": dist(per[:, 1]), "tokens": bd.n_seqs,
+                                    "alg_bytes": abytes_d,
+                                    "note": f"{abytes_d / 1e6:.1f} MB: launch-latency bound; "
+                                            "no roofline claim"},
+        "mixed_attention": {"ms": dist(per[:, 2]), "alg_flops": pflops + dflops,
+                            "alg_bytes": pbytes + dbytes,
+                            "TFLOP_s": (pflops + dflops) / t_mixed / 1e12,
+                            "ideal_ms": ideal_mixed * 1e3, "frac_of_ideal": ideal_mixed / t_mixed},
+        "separate_launches": {
+            "step_ms": dist(step_s),
+            "prefill_attention": {"ms": dist(per_s[:, 2]), "alg_flops": pflops,
+                                  "TFLOP_s": pflops / t_pre / 1e12,
+                                  "frac_mfma": pflops / t_pre / 1e12 / PEAK_BF16_TFLOPS},
+            "decode_attention": {"ms": dist(per_s[:, 3]), "alg_bytes": dbytes,
+                                 "GB_s": dbytes / t_dec / 1e9,
+                                 "frac_hbm": dbytes / t_dec / 1e9 / PEAK_HBM_GBS}},
     }
-    roof = {"bound": "mfma", "achieved": flops / t_pre / 1e12, "peak": PEAK_BF16_TFLOPS,
-            "unit": "TFLOP/s", "frac": flops / t_pre / 1e12 / PEAK_BF16_TFLOPS,
-            "traffic": traffic_from_profiles("prefill")}
+    achieved = (pflops + dflops) / t_mixed / 1e12
+    roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic_from_profiles("mixed"),
+            "kernel": "mixed_kernel (pkv_mixed_attention: order + fused prefill/decode + merge)"}
+    t_step = med(step)
     res = {
         "metric": METRIC,
-        "value": B / step_wall,
+        "value": B / t_step,
         "unit": "tuples/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms,
+        "ms_per_step": t_step * 1e3,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) bf16; no dataset)",
-        "config": {"workload": spec.name, "tuples": B, "q_heads": wl.hq, "kv_heads": wl.hkv,
-                   "head_dim": wl.d, "block_size": 16, "prefix": "U[256,1024]",
-                   "new_tokens": "U[64,256]", "new_tokens_total": T,
-                   "pool_blocks": case.num_blocks, "seed": case.seed,
-                   "step": "kv_append -> prefill_attention -> kv_append(1) -> decode_attention"},
-        "prefill_tflops": kernels["prefill_attention"]["TFLOP_s"],
-        "decode_gbps": kernels["decode_attention"]["GB_s"],
-        "tuples_per_s_gpu_time": B / step_gpu,
+        "config": {"workload": spec.name, "prefill_tuples": bp.n_seqs,
+                   "decode_sequences": bd.n_seqs, "q_heads": wl.hq, "kv_heads": wl.hkv,
+                   "head_dim": wl.d, "block_size": 16, "prefix": "U[512,2048]",
+                   "new_tokens": "U[128,512]", "decode_context": "U[256,4096]",
+                   "new_tokens_total": Tp, "pool_blocks": wl.case.num_blocks,
+                   "seed": wl.case.seed,
+                   "step": "kv_append(suffixes) -> kv_append(decode tokens) -> "
+                           "mixed_attention(prefill + decode)",
+                   "timing": f"median of {args.steps} event-timed steps; "
+                             f"{FLUSH_BYTES >> 20} MiB read between steps, outside the events"},
+        "step_ms": dist(step),
+        "wall_ms_per_step_with_flush": wall * 1e3,
+        "prefill_tflops": pflops / t_pre / 1e12,
+        "decode_gbps": dbytes / t_dec / 1e9,
         "kernels": kernels,
         "roofline": roof,
         "host_allocator_ms": wl.alloc_s * 1e3,
     }
-    return res, wl, dec
+    return res, wl
 
 
-def cpu_baseline(wl, dec, budget_s=15.0):
-    """The oracle on the host cores, on a bounded sample of the same tuples: each sampled
-    tuple runs the same step (prefill of its suffix, then the first decode token)."""
+def cpu_baseline(wl, budget_s=15.0):
+    """The oracle on the host cores over a bounded sample of the primary step's sequences,
+    in the batch's proportion: prefill tuple k (its suffix over its cached prefix), then
+    decode sequences 3k .. 3k+2 (one token over its context), until the budget is spent."""
+    import contextlib
     import oracle
     from tests.gpu_util import sub_pool_for, to_host_bits
     try:
@@ -310,43 +390,102 @@ def cpu_baseline(wl, dec, budget_s=15.0):
     except Exception:  # pragma: no cover
         threadpool_limits = None
     cores = len(os.sched_getaffinity(0))
-    b, _ = wl.batches[0]
-    q = to_host_bits(b.q)
-    kn, vn = to_host_bits(b.k_new), to_host_bits(b.v_new)
-    dq, dk, dvv = to_host_bits(dec["q"]), to_host_bits(dec["k"]), to_host_bits(dec["v"])
-    done, t_total = 0, 0.0
-    import contextlib
+    (bp, _), (bd, _) = wl.batches
+    ratio = bd.n_seqs // max(bp.n_seqs, 1)
+    q, kn, vn = to_host_bits(bp.q), to_host_bits(bp.k_new), to_host_bits(bp.v_new)
+    dq, dk, dvv = to_host_bits(bd.q), to_host_bits(bd.k_new), to_host_bits(bd.v_new)
+    n_pre = n_dec = 0
+    t_total = 0.0
     limit = threadpool_limits(limits=cores) if threadpool_limits else contextlib.nullcontext()
     with limit:
-        for i in range(b.n_seqs):
-            p, n = int(b.prefix_lens[i]), int(b.new_lens[i])
-            a, e = int(b.cu_new_lens[i]), int(b.cu_new_lens[i + 1])
-            pk, pv, row = sub_pool_for(wl.case.pool_k, wl.case.pool_v, dec["host_tables"][i],
-                                       p + n + 1)
+        for k in range(bp.n_seqs):
+            p, n = int(bp.prefix_lens[k]), int(bp.new_lens[k])
+            a, e = int(bp.cu_new_lens[k]), int(bp.cu_new_lens[k + 1])
+            pk, pv, row = sub_pool_for(wl.case.pool_k, wl.case.pool_v, bp.block_tables[k], p + n)
             t0 = time.perf_counter()
-            o, _ = oracle.prefill_attention(pk, pv, row[None], [p], [0, n], q[a:e], kn[a:e],
-                                            vn[a:e], wl.scale, 16)
-            # decode: the pool now holds prefix + suffix; the oracle appends them itself
-            pk2, pv2 = oracle.kv_append(pk, pv, row[None], [p], [0, n], kn[a:e], vn[a:e], 16)
-            od, _ = oracle.decode_attention(pk2, pv2, row[None], [p + n], dq[i:i + 1],
-                                            dk[i:i + 1], dvv[i:i + 1], wl.scale, 16)
+            oracle.prefill_attention(pk, pv, row[None], [p], [0, n], q[a:e], kn[a:e], vn[a:e],
+                                     wl.scale, 16)
             t_total += time.perf_counter() - t0
-            done += 1
+            n_pre += 1
+            for i in range(ratio * k, min(ratio * (k + 1), bd.n_seqs)):
+                c = int(bd.prefix_lens[i])
+                pk, pv, row = sub_pool_for(wl.case.pool_k, wl.case.pool_v, bd.block_tables[i],
+                                           c + 1)
+                t0 = time.perf_counter()
+                oracle.decode_attention(pk, pv, row[None], [c], dq[i:i + 1], dk[i:i + 1],
+                                        dvv[i:i + 1], wl.scale, 16)
+                t_total += time.perf_counter() - t0
+                n_dec += 1
             if t_total >= budget_s:
                 break
-    return {"value": done / t_total, "unit": "tuples/s", "cores": cores, "kind": "oracle",
-            "sample": f"first {done} of {b.n_seqs} tuples of {wl.spec.name} (prefill of the "
-                      f"suffix + first decode token each), numpy float64, {t_total:.1f} s"}
+    return {"value": (n_pre + n_dec) / t_total, "unit": "tuples/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"{n_pre} of {bp.n_seqs} prefill tuples and {n_dec} of {bd.n_seqs} decode "
+                      f"sequences of {wl.spec.name} (prefill of the suffix / one decode token "
+                      f"each), numpy float64, {t_total:.1f} s"}
 
 
 # ---------------------------------------------------------------------------------------
-# secondary workloads (reported beside the primary line; not the metric's workload)
+# secondary workloads (reported beside the primary line; parity cases of their own)
 # ---------------------------------------------------------------------------------------
-def secondary(args, lib, torch):
+def secondary(args, lib, torch, flush):
     import workloads as W
+    from tests.gpu_util import i32
     out = {}
     stream = torch.cuda.current_stream()
     steps, warm = max(5, args.steps // 2), 2
+
+    # tiny: launch-latency bound, reported in microseconds
+    spec = W.TINY
+    wl = Workload(spec, lib, torch)
+    b, _ = wl.batches[0]
+    dv = wl.dev[0]
+    pk, pv = wl.case.pool_k, wl.case.pool_v
+    o = torch.empty((b.total_new, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
+    fns = [lambda: lib.pkv_kv_append(pk, pv, b.k_new, b.v_new, dv["tables"], dv["cached"],
+                                     dv["cu"], dv["max_new"]),
+           lambda: lib.pkv_prefill_attention(pk, pv, b.q, dv["tables"], dv["cached"], dv["cu"],
+                                             dv["max_new"], dv["max_total"], wl.scale, o)]
+    _, step, per = time_steps(torch, stream, fns, steps, warm, flush)
+    out[spec.name] = {"step_us": dist(step, 1e6), "append_us": dist(per[:, 0], 1e6),
+                      "prefill_us": dist(per[:, 1], 1e6),
+                      "note": "launch-latency bound (34 MFLOP); no roofline claim"}
+    del wl, pk, pv
+
+    # Llama-3-8B prefix-reuse prefill step (+ the first decode step)
+    spec = W.LLAMA3_8B_PREFILL
+    wl = Workload(spec, lib, torch)
+    b, _ = wl.batches[0]
+    dv = wl.dev[0]
+    pk, pv = wl.case.pool_k, wl.case.pool_v
+    T, B = b.total_new, b.n_seqs
+    o = torch.empty((T, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
+    dec = wl.decode_followup(0, lib, torch)
+    do = torch.empty((B, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
+    ws = lib.alloc_workspace(lib.pkv_decode_workspace_bytes(B, wl.hq, wl.hkv, wl.d,
+                                                            dec["max_len"]))
+    fns = [lambda: lib.pkv_kv_append(pk, pv, b.k_new, b.v_new, dv["tables"], dv["cached"],
+                                     dv["cu"], dv["max_new"]),
+           lambda: lib.pkv_prefill_attention(pk, pv, b.q, dv["tables"], dv["cached"], dv["cu"],
+                                             dv["max_new"], dv["max_total"], wl.scale, o),
+           lambda: lib.pkv_kv_append(pk, pv, dec["k"], dec["v"], dec["tables"], dec["ctx"],
+                                     dec["cu"], 1),
+           lambda: lib.pkv_decode_attention(pk, pv, dec["q"], dec["tables"], dec["seq_lens"],
+                                            dec["max_len"], wl.scale, do, workspace=ws)]
+    _, step, per = time_steps(torch, stream, fns, steps, warm, flush)
+    flops = prefill_flops(b.prefix_lens, b.new_lens, wl.hq, wl.d)
+    abytes = append_bytes(T, wl.hkv, wl.d)
+    dbytes = decode_bytes(dec["host_ctx"] + 1, wl.hq, wl.hkv, wl.d)
+    tp, ta, td = med(per[:, 1]), med(per[:, 0]), med(per[:, 3])
+    out[spec.name] = {"step_ms": dist(step), "tuples_per_s": B / med(step),
+                      "append_ms": dist(per[:, 0]), "append_GB_s": abytes / ta / 1e9,
+                      "append_frac_hbm": abytes / ta / 1e9 / PEAK_HBM_GBS,
+                      "prefill_ms": dist(per[:, 1]), "prefill_TFLOP_s": flops / tp / 1e12,
+                      "prefill_frac_mfma": flops / tp / 1e12 / PEAK_BF16_TFLOPS,
+                      "decode_token_append_us": dist(per[:, 2], 1e6),
+                      "decode_ms": dist(per[:, 3]), "decode_GB_s": dbytes / td / 1e9,
+                      "decode_frac_hbm": dbytes / td / 1e9 / PEAK_HBM_GBS}
+    del wl, pk, pv, dec
 
     # paged decode, Llama-3-8B layer
     spec = W.LLAMA3_8B_DECODE
@@ -356,7 +495,6 @@ def secondary(args, lib, torch):
     pk, pv = wl.case.pool_k, wl.case.pool_v
     B = b.n_seqs
     seq_lens = b.prefix_lens + 1
-    from tests.gpu_util import i32
     sl = i32(seq_lens)
     maxl = int(seq_lens.max())
     o = torch.empty((B, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
@@ -365,57 +503,14 @@ def secondary(args, lib, torch):
                                      dv["cu"], 1),
            lambda: lib.pkv_decode_attention(pk, pv, b.q, dv["tables"], sl, maxl, wl.scale, o,
                                             workspace=ws)]
-    _, gpu, per = time_events(torch, stream, fns, steps, warm)
+    _, step, per = time_steps(torch, stream, fns, steps, warm, flush)
     dbytes = decode_bytes(seq_lens, wl.hq, wl.hkv, wl.d)
-    out[spec.name] = {"append_us": per[0] * 1e6, "decode_ms": per[1] * 1e3,
-                      "decode_GB_s": dbytes / per[1] / 1e9,
-                      "decode_frac_hbm": dbytes / per[1] / 1e9 / PEAK_HBM_GBS,
-                      "tuples_per_s": B / gpu}
+    td = med(per[:, 1])
+    out[spec.name] = {"append_us": dist(per[:, 0], 1e6), "decode_ms": dist(per[:, 1]),
+                      "decode_GB_s": dbytes / td / 1e9,
+                      "decode_frac_hbm": dbytes / td / 1e9 / PEAK_HBM_GBS,
+                      "tuples_per_s": B / med(step)}
     del wl, pk, pv
-    torch.cuda.empty_cache()
-
-    # mixed 70B-shaped layer: append(all new tokens) -> prefill(128) -> decode(384)
-    spec = W.MIXED_70B
-    wl = Workload(spec, lib, torch)
-    (bp, _), (bd, _) = wl.batches
-    dp, dd = wl.dev
-    pk, pv = wl.case.pool_k, wl.case.pool_v
-    Tp = bp.total_new
-    op = torch.empty((Tp, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
-    od = torch.empty((bd.n_seqs, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
-    sl = i32(bd.prefix_lens + 1)
-    maxl = int(bd.prefix_lens.max()) + 1
-    ws = lib.alloc_workspace(lib.pkv_decode_workspace_bytes(bd.n_seqs, wl.hq, wl.hkv, wl.d,
-                                                            maxl))
-    fns = [lambda: lib.pkv_kv_append(pk, pv, bp.k_new, bp.v_new, dp["tables"], dp["cached"],
-                                     dp["cu"], dp["max_new"]),
-           lambda: lib.pkv_kv_append(pk, pv, bd.k_new, bd.v_new, dd["tables"], dd["cached"],
-                                     dd["cu"], 1),
-           lambda: lib.pkv_prefill_attention(pk, pv, bp.q, dp["tables"], dp["cached"],
-                                             dp["cu"], dp["max_new"], dp["max_total"],
-                                             wl.scale, op),
-           lambda: lib.pkv_decode_attention(pk, pv, bd.q, dd["tables"], sl, maxl, wl.scale,
-                                            od, workspace=ws)]
-    _, gpu, per = time_events(torch, stream, fns, steps, warm)
-    # the same set with prefill and decode fused into one mixed launch
-    fused = fns[:2] + [lambda: lib.pkv_mixed_attention(
-        pk, pv, wl.scale, bp.q, dp["tables"], dp["cached"], dp["cu"], dp["max_new"],
-        dp["max_total"], op, bd.q, dd["tables"], sl, maxl, od, workspace=ws)]
-    _, gpu_f, per_f = time_events(torch, stream, fused, steps, warm)
-    flops = prefill_flops(bp.prefix_lens, bp.new_lens, wl.hq, wl.d)
-    dbytes = decode_bytes(bd.prefix_lens + 1, wl.hq, wl.hkv, wl.d)
-    abytes = append_bytes(Tp, wl.hkv, wl.d)
-    out[spec.name] = {"append_ms": per[0] * 1e3, "append_GB_s": abytes / per[0] / 1e9,
-                      "append_decode_us": per[1] * 1e6,
-                      "prefill_ms": per[2] * 1e3, "prefill_TFLOP_s": flops / per[2] / 1e12,
-                      "prefill_frac_mfma": flops / per[2] / 1e12 / PEAK_BF16_TFLOPS,
-                      "decode_ms": per[3] * 1e3, "decode_GB_s": dbytes / per[3] / 1e9,
-                      "decode_frac_hbm": dbytes / per[3] / 1e9 / PEAK_HBM_GBS,
-                      "set_ms": gpu * 1e3, "sequences_per_s": (bp.n_seqs + bd.n_seqs) / gpu,
-                      "mixed_launch_ms": per_f[2] * 1e3, "set_with_mixed_launch_ms": gpu_f * 1e3,
-                      "sequences_per_s_mixed_launch": (bp.n_seqs + bd.n_seqs) / gpu_f}
-    del wl, pk, pv
-    torch.cuda.empty_cache()
 
     # long documents with a shared 512-token prompt
     spec = W.LONG_DOC_SHARED_PROMPT
@@ -428,19 +523,21 @@ def secondary(args, lib, torch):
                                      dv["cu"], dv["max_new"]),
            lambda: lib.pkv_prefill_attention(pk, pv, b.q, dv["tables"], dv["cached"], dv["cu"],
                                              dv["max_new"], dv["max_total"], wl.scale, o)]
-    _, gpu, per = time_events(torch, stream, fns, steps, warm)
+    _, step, per = time_steps(torch, stream, fns, steps, warm, flush)
     flops = prefill_flops(b.prefix_lens, b.new_lens, wl.hq, wl.d)
     abytes = append_bytes(b.total_new, wl.hkv, wl.d)
-    out[spec.name] = {"append_ms": per[0] * 1e3, "append_GB_s": abytes / per[0] / 1e9,
-                      "prefill_ms": per[1] * 1e3, "prefill_TFLOP_s": flops / per[1] / 1e12,
-                      "prefill_frac_mfma": flops / per[1] / 1e12 / PEAK_BF16_TFLOPS,
-                      "tuples_per_s": b.n_seqs / gpu}
+    ta, tp = med(per[:, 0]), med(per[:, 1])
+    out[spec.name] = {"append_ms": dist(per[:, 0]), "append_GB_s": abytes / ta / 1e9,
+                      "append_frac_hbm": abytes / ta / 1e9 / PEAK_HBM_GBS,
+                      "prefill_ms": dist(per[:, 1]), "prefill_TFLOP_s": flops / tp / 1e12,
+                      "prefill_frac_mfma": flops / tp / 1e12 / PEAK_BF16_TFLOPS,
+                      "tuples_per_s": b.n_seqs / med(step)}
     del wl, pk, pv
     torch.cuda.empty_cache()
     return out
 
 
-def reuse_vs_recompute(args, lib, torch):
+def reuse_vs_recompute(args, lib, torch, flush=None):
     """Kernel-level analog of the paper's prefix reuse (Section 2.1): one downstream attention
     layer with the cached prefix reused (append the N new tokens, prefill them over P cached
     ones) against the same layer recomputed from scratch (append all P + N tokens, prefill all
@@ -479,8 +576,8 @@ def reuse_vs_recompute(args, lib, torch):
         reuse = [lambda: lib.pkv_kv_append(pk, pv, ks, vs, tables, cached, cu_n, maxn),
                  lambda: lib.pkv_prefill_attention(pk, pv, qs, tables, cached, cu_n, maxn, maxl,
                                                    scale, o_u)]
-        _, g_r, per_r = time_events(torch, stream, recompute, steps, warm)
-        _, g_u, per_u = time_events(torch, stream, reuse, steps, warm)
+        _, g_r, per_r = time_events(torch, stream, recompute, steps, warm, flush)
+        _, g_u, per_u = time_events(torch, stream, reuse, steps, warm, flush)
         f_r = prefill_flops(np.zeros_like(L), L, hq, d)
         f_u = prefill_flops(P, N, hq, d)
         res = {"tuples": int(len(L)), "mean_prefix": float(P.mean()), "mean_new": float(N.mean()),
@@ -622,7 +719,7 @@ def profile_mixed(args, lib, torch, wl):
                                          dp["cu"], dp["max_new"], dp["max_total"], op, bd.q,
                                          dd["tables"], sl, maxl, od, workspace=ws)
     stream = torch.cuda.current_stream()
-    _, gpu, per = time_events(torch, stream, [fn], args.steps, args.warmup)
+    _, gpu, per = time_events(torch, stream, [fn], args.steps, args.warmup, Flush(torch))
     print(json.dumps({"workload": wl.spec.name, "kernel": "mixed",
                       "launches": args.steps + args.warmup, "avg_ms": per[0] * 1e3}),
           flush=True)
@@ -666,7 +763,7 @@ def profile_kernel(args, lib, torch):
         fn = lambda: lib.pkv_decode_attention(pk, pv, b.q, dv["tables"], sl, maxl, wl.scale,
                                               out, workspace=ws)
     stream = torch.cuda.current_stream()
-    _, gpu, per = time_events(torch, stream, [fn], args.steps, args.warmup)
+    _, gpu, per = time_events(torch, stream, [fn], args.steps, args.warmup, Flush(torch))
     print(json.dumps({"workload": spec.name, "kernel": args.profile_kernel,
                       "launches": args.steps + args.warmup, "avg_ms": per[0] * 1e3}),
           flush=True)
@@ -680,7 +777,7 @@ def main():
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-kernel", choices=("prefill", "decode", "append", "copy", "mixed"))
-    ap.add_argument("--workload", default="llama3_8b_prefix_reuse_prefill")
+    ap.add_argument("--workload", default=PRIMARY)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this path needs no collective and runs one "
@@ -695,26 +792,76 @@ def main():
     if args.profile_kernel:
         profile_kernel(args, lib, torch)
         return
-    log(f"[bench] primary workload, steps={args.steps} warmup={args.warmup}")
-    res, wl, dec = primary(args, lib, torch)
+    flush = Flush(torch)
+    log(f"[bench] primary workload {PRIMARY}, steps={args.steps} warmup={args.warmup}")
+    res, wl = primary(args, lib, torch, flush)
     log(f"[bench] primary done: {res['ms_per_step']:.3f} ms/step")
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle) ...")
-        res["cpu_baseline"] = cpu_baseline(wl, dec)
+        res["cpu_baseline"] = cpu_baseline(wl)
         log("[bench] cpu baseline done")
     else:
         res["cpu_baseline"] = None
-    del wl, dec
+    del wl
     torch.cuda.empty_cache()
     if not args.no_secondary:
         log("[bench] secondary workloads ...")
-        res["secondary"] = secondary(args, lib, torch)
-        res["secondary"]["reuse_vs_recompute"] = reuse_vs_recompute(args, lib, torch)
+        res["secondary"] = secondary(args, lib, torch, flush)
+        res["secondary"]["reuse_vs_recompute"] = reuse_vs_recompute(args, lib, torch, flush)
         res["secondary"]["achievable_peaks"] = achievable_peaks(torch)
         log("[bench] pipelines under the scheduler ...")
         res["secondary"]["pipelines"] = pipelines(args, lib, torch)
         log("[bench] secondary done")
     print(json.dumps(res), flush=True)
+    summary(res)
+
+
+def summary(res):
+    """The figures of every workload on a few stderr lines (the JSON line is long)."""
+    k = res["kernels"]
+    sep = k["separate_launches"]
+    log(f"[summary] {PRIMARY}: {res['value']:.0f} seq/s, step {res['ms_per_step']:.3f} ms "
+        f"(p10 {res['step_ms']['p10']:.3f}, p90 {res['step_ms']['p90']:.3f}); mixed launch "
+        f"{k['mixed_attention']['ms']['median']:.3f} ms = {res['roofline']['achieved']:.0f} TFLOP/s "
+        f"({100 * res['roofline']['frac']:.1f}% of bf16 peak); separate: prefill "
+        f"{sep['prefill_attention']['ms']['median']:.3f} ms ({sep['prefill_attention']['TFLOP_s']:.0f} "
+        f"TF, {100 * sep['prefill_attention']['frac_mfma']:.1f}%), decode "
+        f"{sep['decode_attention']['ms']['median']:.3f} ms ({sep['decode_attention']['GB_s']:.0f} GB/s, "
+        f"{100 * sep['decode_attention']['frac_hbm']:.1f}%); suffix append "
+        f"{k['kv_append_suffixes']['ms']['median']:.3f} ms ({100 * k['kv_append_suffixes']['frac_hbm']:.1f}%)")
+    cb = res.get("cpu_baseline")
+    if cb:
+        log(f"[summary] cpu oracle: {cb['value']:.2f} seq/s on {cb['cores']} cores")
+    sec = res.get("secondary")
+    if not sec:
+        return
+    t = sec.get("tiny_prefix_reuse_prefill")
+    if t:
+        log(f"[summary] tiny: step {t['step_us']['median']:.1f} us (append "
+            f"{t['append_us']['median']:.1f}, prefill {t['prefill_us']['median']:.1f})")
+    s = sec.get("llama3_8b_prefix_reuse_prefill")
+    if s:
+        log(f"[summary] llama3_8b prefix reuse: {s['tuples_per_s']:.0f} tuples/s, prefill "
+            f"{s['prefill_ms']['median']:.3f} ms ({100 * s['prefill_frac_mfma']:.1f}%), append "
+            f"{100 * s['append_frac_hbm']:.1f}% HBM, decode {100 * s['decode_frac_hbm']:.1f}% HBM")
+    s = sec.get("llama3_8b_paged_decode")
+    if s:
+        log(f"[summary] llama3_8b decode: {s['decode_ms']['median']:.3f} ms "
+            f"({s['decode_GB_s']:.0f} GB/s, {100 * s['decode_frac_hbm']:.1f}%), append "
+            f"{s['append_us']['median']:.1f} us")
+    s = sec.get("long_doc_shared_prompt")
+    if s:
+        log(f"[summary] long docs: prefill {s['prefill_ms']['median']:.3f} ms "
+            f"({s['prefill_TFLOP_s']:.0f} TF, {100 * s['prefill_frac_mfma']:.1f}%), append "
+            f"{s['append_ms']['median'] * 1e3:.1f} us ({100 * s['append_frac_hbm']:.1f}%)")
+    r = sec.get("reuse_vs_recompute")
+    if r:
+        log("[summary] reuse vs recompute: " + ", ".join(
+            f"{n} {v['speedup']:.2f}x" for n, v in r.items()))
+    a = sec.get("achievable_peaks")
+    if a:
+        log(f"[summary] achievable: bf16 GEMM {a['gemm_bf16_8192_TFLOP_s']:.0f} TF, copy "
+            f"{a['copy_1GiB_GB_s']:.0f} GB/s")
 
 
 if __name__ == "__main__":

@@ -20,13 +20,30 @@
  *   - Supported shapes: block_size 16; head_dim 64 or 128; num_q_heads a multiple of
  *     num_kv_heads; decode additionally needs num_q_heads / num_kv_heads <= 16. Anything else
  *     returns PKV_ERR_UNSUPPORTED_SHAPE. Zero sequences or zero tokens is a successful no-op.
- *   - Device calls take device pointers (caller-owned; the library never allocates or frees
- *     device memory) and a hipStream_t passed as void* (NULL = the null stream). They are
- *     asynchronous; results are ready when the stream has drained. A launch failure returns
- *     PKV_ERR_HIP with hipGetErrorString's text. Device calls are reentrant.
- *   - The contents of device metadata (block ids within the pool, lengths within the table)
- *     are the caller's contract: the host cannot check them without a device-to-host copy.
- *     Every kernel bounds the table index it computes by max_blocks and skips -1 entries.
+ *   - Device calls take device pointers (caller-owned) and a hipStream_t passed as void*
+ *     (NULL = the null stream). They never allocate or free device memory (the decode's
+ *     workspace is the caller's, or the fixed scratch of pkv_decode_attention_noalloc); the
+ *     one call that does is pkv_sched_run in device mode, which allocates its own metadata,
+ *     output and workspace buffers for the run and frees them before returning. Device calls
+ *     are asynchronous; results are ready when the stream has drained. A launch failure
+ *     returns PKV_ERR_HIP with hipGetErrorString's text. Device calls are reentrant.
+ *   - The contents of device metadata (block ids within the pool, lengths within the host
+ *     maxima and the table, monotone token offsets) are the caller's contract: the host cannot
+ *     check them without a device-to-host copy. The kernels only bound what they index (a
+ *     table index by max_blocks; an id outside the pool reads a stand-in block; a length past
+ *     the planned launch is cut), so bad metadata gives finite but wrong results, never an
+ *     access outside the pool, the table or the workspace. Opt-in checking: with
+ *     PKV_DEBUG_VALIDATE set in the environment (any value but "0"), or after
+ *     pkv_set_debug_validate(1), every device call first runs a validation kernel over its
+ *     metadata, waits for the stream, and returns PKV_ERR_BAD_METADATA (launching nothing
+ *     else) naming what failed and the first offending sequence. This synchronises every
+ *     call: a debugging aid, not for graph capture or timed runs.
+ *   - Interface choices: the block pool is host bookkeeping only (it takes the order in which
+ *     blocks are handed out, not device pointers or a seed; the caller allocates the K/V
+ *     tensors); device calls take host maxima (max_new_len, max_total_len, max_seq_len,
+ *     max_len) that size the launch without a device-to-host read; the pool layout below is
+ *     chunk-major K and dim-major V rather than row-major slabs; prefill needs no workspace
+ *     (pkv_prefill_workspace_bytes returns 0 and keeps its arguments for future kernels).
  *   - bf16 is IEEE binary16 "brain float" (1 sign, 8 exponent, 7 mantissa bits), stored as
  *     16-bit words.
  *
@@ -58,7 +75,8 @@ typedef enum {
   PKV_ERR_UNSUPPORTED_SHAPE = 4,  /* block_size / head_dim / head ratio not supported */
   PKV_ERR_NOT_FOUND = 5,          /* unknown sequence id */
   PKV_ERR_HIP = 6,                /* a HIP runtime call or launch failed */
-  PKV_ERR_KEY_EXISTS = 7          /* prefix publish refused: the key is already cached */
+  PKV_ERR_KEY_EXISTS = 7,         /* prefix publish refused: the key is already cached */
+  PKV_ERR_BAD_METADATA = 8        /* PKV_DEBUG_VALIDATE refused a call's device metadata */
 } pkv_status;
 
 /* Message of this thread's last failed call ("" if none). */
@@ -66,6 +84,11 @@ const char* pkv_last_error(void);
 
 /* ABI version, bumped on any incompatible change. */
 int32_t pkv_abi_version(void);
+
+/* Turn the opt-in metadata validation on (non-zero) or off for the process (see Conventions);
+ * overrides PKV_DEBUG_VALIDATE. pkv_get_debug_validate returns the current setting. */
+pkv_status pkv_set_debug_validate(int32_t on);
+int32_t pkv_get_debug_validate(void);
 
 /* ---------------------------------------------------------------------------------------
  * Block pool: host-side bookkeeping of which physical blocks each sequence (tuple) holds.
@@ -410,6 +433,27 @@ typedef struct {
  * are overwritten. The run allocates its own metadata, output and workspace buffers and frees
  * them before returning. */
 typedef struct {
+  int64_t step;            /* engine step */
+  int32_t phase;           /* 0: before the group's KV append (every earlier launch has completed
+                              and the metadata is on the device); 1: after its attention */
+  int32_t decode;          /* 1: a decode group (one new token each), 0: a prefill group */
+  int32_t num_seqs;
+  int32_t max_blocks;
+  const int32_t* tables;   /* host [num_seqs][max_blocks]: the block tables the launches use */
+  const int32_t* cached;   /* host [num_seqs]: tokens in the pool before the append */
+  const int32_t* cu_new;   /* host [num_seqs + 1]: sequence k appends rows cu_new[k] .. of k_src /
+                              v_src; a prefill group's queries are the same rows of q_src, a
+                              decode group's query of sequence k is row k */
+  const void* out;         /* device bf16 [rows][num_q_heads][head_dim]: the group's attention
+                              output (prefill: row per new token; decode: row per sequence),
+                              valid in phase 1 */
+} pkv_sched_group;
+/* Optional observer of device mode (tests, tracing): called on the calling thread twice per
+ * group of sequences launched together, with the stream drained; it may read the pool and the
+ * output but must not modify them. */
+typedef void (*pkv_sched_group_hook)(void* user, const pkv_sched_group* group);
+
+typedef struct {
   pkv_paged_kv kv;
   int32_t num_q_heads;
   const void* q_src;
@@ -417,6 +461,8 @@ typedef struct {
   const void* v_src;
   int32_t src_rows;
   void* stream;
+  pkv_sched_group_hook group_hook;  /* NULL: none */
+  void* hook_user;
 } pkv_sched_device;
 
 typedef struct {
@@ -427,7 +473,9 @@ typedef struct {
   int64_t cow_copies, evictions, outputs;
   int64_t prefill_chunks;  /* prompt pieces prefilled (one per prompt without a budget) */
   int32_t max_batch;       /* largest batch the engine ran */
-  double gpu_ms;           /* device mode: GPU time of all steps (events); 0 otherwise */
+  double gpu_ms;           /* device mode: GPU time of the steps' launches (events around the
+                              block copies, appends and attention; not the metadata uploads or
+                              the host's work between launches); 0 otherwise */
   double wall_ms;          /* host wall time of the run */
 } pkv_sched_stats;
 

@@ -18,7 +18,7 @@ LIB = os.path.join(PKG, "libpkv.so")
 ARCH = "gfx950"
 
 SOURCES = ["pool.cpp", "sched.cpp", "api.cpp", "kv_copy.hip", "block_copy.hip", "decode.hip",
-           "prefill.hip", "mixed.hip"]
+           "prefill.hip", "mixed.hip", "validate.hip"]
 
 
 def hipcc() -> str:

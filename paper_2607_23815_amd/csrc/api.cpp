@@ -2,6 +2,9 @@
 // Every check happens before any launch, so a refused call has enqueued nothing.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
+#include <cstdlib>
+#include <cstring>
 #include <string>
 
 #include "internal.h"
@@ -55,6 +58,60 @@ pkv_status launched(hipError_t err, const char* fn) {
   if (err != hipSuccess)
     return fail(PKV_ERR_HIP, std::string(fn) + ": " + hipGetErrorString(err));
   return ok();
+}
+
+// Opt-in validation of device metadata: off unless PKV_DEBUG_VALIDATE is set (and not "0")
+// in the environment when the library first needs the setting, or pkv_set_debug_validate
+// turns it on.
+std::atomic<int> g_debug_validate{-1};
+
+bool debug_validate() {
+  int v = g_debug_validate.load(std::memory_order_relaxed);
+  if (v < 0) {
+    const char* e = std::getenv("PKV_DEBUG_VALIDATE");
+    v = (e != nullptr && e[0] != '\0' && std::strcmp(e, "0") != 0) ? 1 : 0;
+    int expected = -1;
+    g_debug_validate.compare_exchange_strong(expected, v);
+    v = g_debug_validate.load(std::memory_order_relaxed);
+  }
+  return v == 1;
+}
+
+// With validation on: run the checks (waiting for the stream) and refuse the call if any
+// fails; with it off: nothing.
+pkv_status check_metadata(const char* fn, const MetaCheck* checks, int n, hipStream_t stream) {
+  if (!debug_validate()) return PKV_OK;
+  uint32_t bad = 0u;
+  int32_t seq = -1, which = -1;
+  const hipError_t err = validate_metadata(checks, n, stream, &bad, &seq, &which);
+  if (err != hipSuccess) return fail(PKV_ERR_HIP, std::string(fn) + ": " + hipGetErrorString(err));
+  if (bad == 0u) return PKV_OK;
+  std::string what;
+  if (bad & kMetaBadBlockId) what += " a block id outside the pool;";
+  if (bad & kMetaBadLength) what += " a length outside its host maximum or the table;";
+  if (bad & kMetaBadOffsets) what += " token offsets not starting at 0, decreasing or not ending at the total;";
+  std::string batch;
+  if (n > 1) batch = which == 0 ? " of the prefill batch" : " of the decode batch";
+  return fail(PKV_ERR_BAD_METADATA, std::string(fn) + ": PKV_DEBUG_VALIDATE refused the call:" +
+                                        what + " first offending sequence " +
+                                        std::to_string(seq) + batch);
+}
+
+MetaCheck meta(int32_t mode, const KvView& view, const int32_t* tables, int32_t max_blocks,
+               const int32_t* lens, const int32_t* cu, int32_t num_seqs, int64_t total,
+               int64_t max_len, int64_t max_total) {
+  MetaCheck c;
+  c.mode = mode;
+  c.tables = tables;
+  c.max_blocks = max_blocks;
+  c.num_blocks = view.num_blocks;
+  c.lens = lens;
+  c.cu = cu;
+  c.num_seqs = num_seqs;
+  c.total = total;
+  c.max_len = max_len;
+  c.max_total = max_total;
+  return c;
 }
 
 // Argument checks of a prefill batch (prefill and mixed calls); *empty when there is nothing
@@ -151,7 +208,14 @@ extern "C" {
 
 const char* pkv_last_error(void) { return pkv::g_last_error.c_str(); }
 
-int32_t pkv_abi_version(void) { return 1; }
+int32_t pkv_abi_version(void) { return 2; }
+
+pkv_status pkv_set_debug_validate(int32_t on) {
+  g_debug_validate.store(on != 0 ? 1 : 0, std::memory_order_relaxed);
+  return ok();
+}
+
+int32_t pkv_get_debug_validate(void) { return debug_validate() ? 1 : 0; }
 
 pkv_status pkv_kv_append(const pkv_paged_kv* kv, const void* k_new, const void* v_new,
                          const int32_t* block_tables, int32_t max_blocks,
@@ -174,6 +238,12 @@ pkv_status pkv_kv_append(const pkv_paged_kv* kv, const void* k_new, const void* 
     return fail(PKV_ERR_INVALID_ARG, "pkv_kv_append: max_new_len and max_blocks must be > 0");
   if (num_seqs > kMaxGridZ)
     return fail(PKV_ERR_INVALID_ARG, "pkv_kv_append: more than 65535 sequences per call");
+  {
+    const MetaCheck c = meta(kMetaAppend, view, block_tables, max_blocks, cached_lens,
+                             cu_new_lens, num_seqs, total_new, max_new_len,
+                             (int64_t)max_blocks * kSupportedBlockSize);
+    if ((st = check_metadata(fn, &c, 1, static_cast<hipStream_t>(stream))) != PKV_OK) return st;
+  }
   return launched(launch_kv_append(view, static_cast<const uint16_t*>(k_new),
                                    static_cast<const uint16_t*>(v_new), block_tables,
                                    max_blocks, cached_lens, cu_new_lens, num_seqs, max_new_len,
@@ -204,6 +274,11 @@ pkv_status pkv_prefill_attention(const pkv_paged_kv* kv, const void* q, int32_t 
                      cu_new_lens, num_seqs, total_new, max_new_len, max_total_len, scale, out,
                      workspace, workspace_bytes, &empty);
   if (st != PKV_OK || empty) return st;
+  {
+    const MetaCheck c = meta(kMetaPrefill, view, block_tables, max_blocks, cached_lens,
+                             cu_new_lens, num_seqs, total_new, max_new_len, max_total_len);
+    if ((st = check_metadata(fn, &c, 1, static_cast<hipStream_t>(stream))) != PKV_OK) return st;
+  }
   return launched(launch_prefill(view, static_cast<const uint16_t*>(q), num_q_heads,
                                  block_tables, max_blocks, cached_lens, cu_new_lens, num_seqs,
                                  max_new_len, scale, static_cast<uint16_t*>(out), lse,
@@ -232,6 +307,11 @@ pkv_status pkv_decode_attention(const pkv_paged_kv* kv, const void* q, int32_t n
   st = check_decode(view, fn, q, num_q_heads, block_tables, max_blocks, seq_lens, num_seqs,
                     max_seq_len, scale, out, workspace, workspace_bytes, &empty);
   if (st != PKV_OK || empty) return st;
+  {
+    const MetaCheck c = meta(kMetaDecode, view, block_tables, max_blocks, seq_lens, nullptr,
+                             num_seqs, -1, max_seq_len, 0);
+    if ((st = check_metadata(fn, &c, 1, static_cast<hipStream_t>(stream))) != PKV_OK) return st;
+  }
   return launched(launch_decode(view, static_cast<const uint16_t*>(q), num_q_heads,
                                 block_tables, max_blocks, seq_lens, num_seqs, max_seq_len, scale,
                                 static_cast<uint16_t*>(out), lse, workspace,
@@ -254,6 +334,11 @@ pkv_status pkv_decode_attention_noalloc(const pkv_paged_kv* kv, const void* q,
   st = check_decode(view, fn, q, num_q_heads, block_tables, max_blocks, seq_lens, num_seqs,
                     max_seq_len, scale, out, nullptr, 0, &empty, /*scratch=*/true);
   if (st != PKV_OK || empty) return st;
+  {
+    const MetaCheck c = meta(kMetaDecode, view, block_tables, max_blocks, seq_lens, nullptr,
+                             num_seqs, -1, max_seq_len, 0);
+    if ((st = check_metadata(fn, &c, 1, static_cast<hipStream_t>(stream))) != PKV_OK) return st;
+  }
   void* ws = nullptr;
   const hipError_t err = decode_scratch(&ws);
   if (err != hipSuccess) return launched(err, fn);
@@ -288,6 +373,14 @@ pkv_status pkv_mixed_attention(const pkv_paged_kv* kv, int32_t num_q_heads, floa
   if (st != PKV_OK) return st;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   if (no_prefill && no_decode) return ok();
+  {
+    MetaCheck c[2];
+    c[0] = meta(kMetaPrefill, view, block_tables, max_blocks, cached_lens, cu_new_lens,
+                no_prefill ? 0 : num_seqs, total_new, max_new_len, max_total_len);
+    c[1] = meta(kMetaDecode, view, d_block_tables, d_max_blocks, seq_lens, nullptr,
+                no_decode ? 0 : d_num_seqs, -1, max_seq_len, 0);
+    if ((st = check_metadata(fn, c, 2, s)) != PKV_OK) return st;
+  }
   if (no_decode)
     return launched(launch_prefill(view, static_cast<const uint16_t*>(q), num_q_heads,
                                    block_tables, max_blocks, cached_lens, cu_new_lens, num_seqs,
@@ -326,6 +419,11 @@ pkv_status pkv_gather_kv(const pkv_paged_kv* kv, const int32_t* block_tables,
     return fail(PKV_ERR_INVALID_ARG, "pkv_gather_kv: outputs must be 16-byte aligned");
   if (num_seqs > kMaxGridZ)
     return fail(PKV_ERR_INVALID_ARG, "pkv_gather_kv: more than 65535 sequences per call");
+  {
+    const MetaCheck c = meta(kMetaGather, view, block_tables, max_blocks, lens, cu_lens,
+                             num_seqs, -1, max_len, 0);
+    if ((st = check_metadata(fn, &c, 1, static_cast<hipStream_t>(stream))) != PKV_OK) return st;
+  }
   return launched(launch_gather_kv(view, block_tables, max_blocks, lens, cu_lens, num_seqs,
                                    max_len, static_cast<uint16_t*>(k_out),
                                    static_cast<uint16_t*>(v_out),

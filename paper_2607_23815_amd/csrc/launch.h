@@ -67,6 +67,31 @@ hipError_t launch_decode(const KvView& kv, const uint16_t* q, int32_t hq,
 constexpr size_t kDecodeScratchBytes = size_t(32) << 20;
 hipError_t decode_scratch(void** ptr);
 
+// Opt-in metadata validation (PKV_DEBUG_VALIDATE). One check per batch of a call: for
+// append / prefill, `lens` are the cached lengths and `cu` the new-token offsets (ending at
+// `total`), each sequence's new tokens at most `max_len` and cached + new at most
+// `max_total`; for decode, `lens` are the sequence lengths (1 .. max_len); for gather, `lens`
+// the gathered lengths (at most max_len, equal to the cu steps). Every table entry the call
+// reads or writes must name a pool block.
+enum : int32_t { kMetaAppend = 0, kMetaPrefill = 1, kMetaDecode = 2, kMetaGather = 3 };
+enum : uint32_t { kMetaBadBlockId = 1u, kMetaBadLength = 2u, kMetaBadOffsets = 4u };
+struct MetaCheck {
+  int32_t mode;
+  const int32_t* tables;
+  int32_t max_blocks;
+  int32_t num_blocks;
+  const int32_t* lens;
+  const int32_t* cu;  // null for decode
+  int32_t num_seqs;
+  int64_t total;      // cu[num_seqs] must equal it (< 0: not checked)
+  int64_t max_len;
+  int64_t max_total;
+};
+// Runs the checks in order on `stream` and waits for each; *bad = the failed check's bits
+// (0 if all pass), *first_seq its lowest offending sequence, *which its index.
+hipError_t validate_metadata(const MetaCheck* checks, int n_checks, hipStream_t stream,
+                             uint32_t* bad, int32_t* first_seq, int32_t* which);
+
 // Mixed launch: a prefill batch (arguments as launch_prefill) and a decode batch (d_*, as
 // launch_decode, with its workspace) in one fused kernel between the decode's ordering
 // kernel and its merge. Both batches must be non-empty.

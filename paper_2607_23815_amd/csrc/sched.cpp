@@ -112,25 +112,28 @@ class DeviceRunner {
     return PKV_OK;
   }
 
-  // Runs one step; adds its GPU time to *ms.
-  pkv_status step(pkv_pool* pool, const std::vector<int32_t>& copies,
+  // Runs one step; adds the GPU time of its launches (block copies, appends, attention; not
+  // the metadata uploads or the host's work between them) to *ms.
+  pkv_status step(pkv_pool* pool, int64_t step_no, const std::vector<int32_t>& copies,
                   const std::vector<StepItem>& pre, const std::vector<StepItem>& dec,
                   double* ms) {
     hipStream_t stream = static_cast<hipStream_t>(dev_.stream);
-    hipError_t e = hipEventRecord(ev0_, stream);
-    if (e != hipSuccess) return hip_fail(e);
+    hipError_t e = hipSuccess;
     int32_t* h = static_cast<int32_t*>(meta_host_);
     int32_t* d = static_cast<int32_t*>(meta_dev_);
     pkv_status st = PKV_OK;
+    step_no_ = step_no;
+    ms_ = ms;
     // copy-on-write copies (one pair per admitted task that continues a partly filled
     // block), in groups of at most max_batch pairs, which the staging area holds
     for (size_t c0 = 0; c0 < copies.size(); c0 += 2 * (size_t)max_batch_) {
       const size_t cn = std::min(copies.size() - c0, 2 * (size_t)max_batch_);
       std::copy(copies.begin() + c0, copies.begin() + c0 + cn, h);
       if ((e = upload(h, d, cn, stream)) != hipSuccess) return hip_fail(e);
+      if ((e = hipEventRecord(ev0_, stream)) != hipSuccess) return hip_fail(e);
       st = pkv_copy_blocks(&dev_.kv, d, (int32_t)(cn / 2), dev_.stream);
       if (st != PKV_OK) return st;
-      if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e);
+      if ((st = end_segment()) != PKV_OK) return st;
     }
     // prefill: groups of at most src_rows new tokens
     size_t a = 0;
@@ -143,17 +146,39 @@ class DeviceRunner {
       a = b;
     }
     if (!dec.empty() && (st = run_group(pool, dec, 0, dec.size(), true)) != PKV_OK) return st;
-    if ((e = hipEventRecord(ev1_, stream)) != hipSuccess) return hip_fail(e);
-    if ((e = hipEventSynchronize(ev1_)) != hipSuccess) return hip_fail(e);
-    float t = 0.f;
-    if ((e = hipEventElapsedTime(&t, ev0_, ev1_)) != hipSuccess) return hip_fail(e);
-    *ms += t;
     return PKV_OK;
   }
 
  private:
   pkv_status hip_fail(hipError_t e) {
     return pkv::fail(PKV_ERR_HIP, std::string("pkv_sched_run: ") + hipGetErrorString(e));
+  }
+
+  // End of a timed segment that began with ev0_: wait for it and add its time.
+  pkv_status end_segment() {
+    hipError_t e = hipEventRecord(ev1_, static_cast<hipStream_t>(dev_.stream));
+    if (e == hipSuccess) e = hipEventSynchronize(ev1_);
+    float t = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&t, ev0_, ev1_);
+    if (e != hipSuccess) return hip_fail(e);
+    *ms_ += t;
+    return PKV_OK;
+  }
+
+  void call_hook(int32_t phase, bool decode, int32_t n, const int32_t* tab, const int32_t* cached,
+                 const int32_t* cu) {
+    if (dev_.group_hook == nullptr) return;
+    pkv_sched_group g;
+    g.step = step_no_;
+    g.phase = phase;
+    g.decode = decode ? 1 : 0;
+    g.num_seqs = n;
+    g.max_blocks = max_table_;
+    g.tables = tab;
+    g.cached = cached;
+    g.cu_new = cu;
+    g.out = out_;
+    dev_.group_hook(dev_.hook_user, &g);
   }
 
   hipError_t upload(const int32_t* h, int32_t* d, size_t n, hipStream_t stream) {
@@ -190,6 +215,11 @@ class DeviceRunner {
     const size_t total = (size_t)n * max_table_ + 3 * (size_t)n + 1;
     hipError_t e = upload(h, d, total, stream);
     if (e != hipSuccess) return hip_fail(e);
+    if (dev_.group_hook != nullptr) {  // the pool and the metadata settle before the hook
+      if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e);
+      call_hook(0, decode, n, h_tab, h_cached, h_cu);
+    }
+    if ((e = hipEventRecord(ev0_, stream)) != hipSuccess) return hip_fail(e);
     const int32_t* d_tab = d;
     const int32_t* d_cached = d_tab + (size_t)n * max_table_;
     const int32_t* d_cu = d_cached + n;
@@ -208,7 +238,8 @@ class DeviceRunner {
                                  d_cached, d_cu, n, rows, max_new, max_total, scale, out_,
                                  nullptr, nullptr, 0, dev_.stream);
     if (st != PKV_OK) return st;
-    if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e);
+    if ((st = end_segment()) != PKV_OK) return st;
+    call_hook(1, decode, n, h_tab, h_cached, h_cu);
     return PKV_OK;
   }
 
@@ -226,6 +257,8 @@ class DeviceRunner {
   }
 
   pkv_sched_device dev_{};
+  int64_t step_no_ = 0;
+  double* ms_ = nullptr;
   int32_t max_table_ = 0, max_batch_ = 0;
   size_t meta_bytes_ = 0, ws_bytes_ = 0;
   void* meta_dev_ = nullptr;
@@ -577,7 +610,7 @@ class Sched {
         done->push_back({running_[k], 1});
     }
     if (dev != nullptr) {
-      pkv_status st = dev->step(pool_, copies_, pre, dec, &stats_.gpu_ms);
+      pkv_status st = dev->step(pool_, step_, copies_, pre, dec, &stats_.gpu_ms);
       if (st != PKV_OK) return st;
     }
     return PKV_OK;

@@ -35,6 +35,7 @@ PKV_ERR_UNSUPPORTED_SHAPE = 4
 PKV_ERR_NOT_FOUND = 5
 PKV_ERR_HIP = 6
 PKV_ERR_KEY_EXISTS = 7
+PKV_ERR_BAD_METADATA = 8
 PKV_EVICT_LRU, PKV_EVICT_MRU = 0, 1
 PKV_PIN_EXPLICIT, PKV_PIN_VIRTUAL = 0, 1
 
@@ -76,15 +77,27 @@ class SchedStats(ctypes.Structure):
                 ("cow_copies", c_int64), ("evictions", c_int64), ("outputs", c_int64),
                 ("prefill_chunks", c_int64), ("max_batch", c_int32), ("gpu_ms", c_double), ("wall_ms", c_double)]
 
+class SchedGroup(ctypes.Structure):
+    _fields_ = [("step", c_int64), ("phase", c_int32), ("decode", c_int32),
+                ("num_seqs", c_int32), ("max_blocks", c_int32), ("tables", P_int32),
+                ("cached", P_int32), ("cu_new", P_int32), ("out", c_void_p)]
+
+
+SCHED_GROUP_HOOK = ctypes.CFUNCTYPE(None, c_void_p, ctypes.POINTER(SchedGroup))
+
+
 class SchedDevice(ctypes.Structure):
     _fields_ = [("kv", PagedKV), ("num_q_heads", c_int32), ("q_src", c_void_p),
                 ("k_src", c_void_p), ("v_src", c_void_p), ("src_rows", c_int32),
-                ("stream", c_void_p)]
+                ("stream", c_void_p), ("group_hook", SCHED_GROUP_HOOK),
+                ("hook_user", c_void_p)]
 
 
 _SIGS = {
     "pkv_last_error": (ctypes.c_char_p, []),
     "pkv_abi_version": (c_int32, []),
+    "pkv_set_debug_validate": (c_int32, [c_int32]),
+    "pkv_get_debug_validate": (c_int32, []),
     "pkv_pool_create": (c_int32, [c_int32, c_int32, P_int32, ctypes.POINTER(c_void_p)]),
     "pkv_pool_destroy": (None, [c_void_p]),
     "pkv_pool_num_free": (c_int32, [c_void_p]),
@@ -159,6 +172,14 @@ def pkv_last_error() -> str:
 
 def pkv_abi_version() -> int:
     return int(_lib.pkv_abi_version())
+
+
+def pkv_set_debug_validate(on: bool) -> None:
+    _check(_lib.pkv_set_debug_validate(1 if on else 0))
+
+
+def pkv_get_debug_validate() -> bool:
+    return bool(_lib.pkv_get_debug_validate())
 
 
 # ----------------------------------------------------------------------------------------
@@ -315,11 +336,14 @@ def sched_config(policy, num_blocks, max_out, alpha=1.0, beta=0.5, delta=0, pinn
 
 
 def pkv_sched_run(cfg: SchedConfig, fanout, suffix, out_len, filtered, device=None,
-                  max_events: int = 0):
+                  max_events: int = 0, group_hook=None):
     """Run a pipeline (per-stage arrays, as the oracle's Pipeline takes them).
     Returns (stats dict, trace int32 [n][5] (None when max_events is 0), final budgets).
     device: None, or a dict(k_cache, v_cache, q_src, k_src, v_src[, stream]) of GPU tensors
-    for device mode."""
+    for device mode. group_hook (device mode): a callable receiving, for every group of
+    sequences launched together, a dict(step, phase, decode, tables, cached, cu_new, out_ptr)
+    with the host metadata as numpy copies (phase 0 before the group's append, 1 after its
+    attention)."""
     S = len(suffix)
     fan = np.ascontiguousarray(np.asarray(list(fanout) + [1] * (S - len(fanout)),
                                           dtype=np.int32)[:S])
@@ -345,6 +369,17 @@ def pkv_sched_run(cfg: SchedConfig, fanout, suffix, out_len, filtered, device=No
         dv.stream = _stream(device.get("stream"))
         if int(device["k_src"].shape[2]) != d:
             raise ValueError("q_src / k_src head dims differ")
+        if group_hook is not None:
+            def _hook(_user, gp):
+                g = gp.contents
+                n, mb = int(g.num_seqs), int(g.max_blocks)
+                group_hook(dict(
+                    step=int(g.step), phase=int(g.phase), decode=bool(g.decode),
+                    tables=np.ctypeslib.as_array(g.tables, shape=(n * mb,)).reshape(n, mb).copy(),
+                    cached=np.ctypeslib.as_array(g.cached, shape=(n,)).copy(),
+                    cu_new=np.ctypeslib.as_array(g.cu_new, shape=(n + 1,)).copy(),
+                    out_ptr=int(g.out or 0)))
+            dv.group_hook = SCHED_GROUP_HOOK(_hook)
         dev_arg = ctypes.byref(dv)
     if not (len(out) == len(suf) == len(flt)):
         raise ValueError("suffix, out_len and filtered must have the same lengths")

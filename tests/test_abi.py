@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported(lib):
     for n in names:
         assert hasattr(raw, n), f"{n} declared in pkv.h but not exported"
     assert set(names) == set(lib.EXPORTED)
-    assert lib.pkv_abi_version() == 1
+    assert lib.pkv_abi_version() == 2
 
 
 def test_no_internal_symbols_leak():
@@ -353,3 +353,39 @@ def test_noalloc_decode_refuses_oversize_calls_on_the_host(lib):
                                           fake, None, None) == lib.PKV_ERR_UNSUPPORTED_SHAPE
     assert L.pkv_decode_attention_noalloc(ctypes.byref(kv), None, 64, None, 0, None, 0, 0, 0.1,
                                           None, None, None) == lib.PKV_OK
+
+
+def test_debug_validate_switch(lib):
+    """The opt-in metadata validation is a process-wide switch (its checks run on the GPU;
+    tests/test_gpu_validate.py covers them)."""
+    was = lib.pkv_get_debug_validate()
+    try:
+        lib.pkv_set_debug_validate(True)
+        assert lib.pkv_get_debug_validate() is True
+        lib.pkv_set_debug_validate(False)
+        assert lib.pkv_get_debug_validate() is False
+    finally:
+        lib.pkv_set_debug_validate(was)
+    # host-side refusals come before validation: a bad call with validation on still returns
+    # INVALID_ARG without touching the GPU
+    L = lib._lib
+    kv = _fake_kv(lib)
+    fake = ctypes.c_void_p(0x3000)
+    lib.pkv_set_debug_validate(True)
+    try:
+        assert L.pkv_kv_append(ctypes.byref(kv), None, fake, fake, 4, fake, fake, 1, 1, 1,
+                               None) == lib.PKV_ERR_INVALID_ARG
+    finally:
+        lib.pkv_set_debug_validate(was)
+
+
+def test_env_switch_is_read_by_a_fresh_process():
+    import subprocess
+    import sys
+    code = ("import sys; sys.path.insert(0, %r); from paper_2607_23815_amd import lib; "
+            "print(int(lib.pkv_get_debug_validate()))" % ROOT)
+    for val, want in (("1", "1"), ("0", "0"), ("", "0")):
+        env = dict(os.environ, PKV_DEBUG_VALIDATE=val)
+        out = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True,
+                             text=True, timeout=120)
+        assert out.stdout.strip().splitlines()[-1] == want, (val, out.stdout, out.stderr)

@@ -164,3 +164,46 @@ def test_decode_over_long_length_is_cut_to_the_planned_splits(gpu_lib, hq, hkv, 
     torch.cuda.synchronize()
     ref = _oracle_first_keys(case, b, np.minimum(lens, cut), scale_for(d))
     check(spec.name, (to_host_bits(out), lse.cpu().numpy().astype(np.float64)), ref)
+
+
+def test_decode_spike_probes_at_long_context(gpu_lib):
+    """Spike keys (parallel to the query, large norm, value 10) decide the output alone when
+    visible: one in the middle of a long context (inside one split of several), one at the
+    step's own appended token (position C), each ~10 after the merge. A spike in the stale
+    slot C + 1 of the last block (never appended) must stay invisible."""
+    import torch
+    say("[decode] spike probes at long context")
+    ctx = [4100, 6000, 9000, 5005]
+    spec = W.WorkloadSpec("decode_spikes", 161, 16, 4, 128,
+                          (W.BatchSpec("decode", len(ctx), W.Dist.const(1), W.Dist.const(1)),),
+                          ("scale", 1.25))
+    case = W.make_case(spec, prefix_override=[ctx])
+    b = case.batches[0]
+    g = case.hq // case.hkv
+    h = 5
+    ten = np.uint16(0x4120)
+
+    def spike_bits(i):
+        qv = bf16_to_f64(b.q[i, h])
+        sp = (qv * (320.0 / np.linalg.norm(qv))).astype(np.float32)
+        return (sp.view(np.uint32) >> 16).astype(np.uint16)
+
+    def plant(i, t):
+        blk, slot = int(b.block_tables[i, t // 16]), t % 16
+        kb = spike_bits(i)
+        case.pool_k[blk, h // g, :, slot, :] = kb.reshape(-1, 8)
+        case.pool_v[blk, h // g, :, slot] = ten
+
+    plant(0, 2049)                      # mid-context, cached
+    b.k_new[1, h // g] = spike_bits(1)  # the appended token itself (position C)
+    b.v_new[1, h // g] = ten
+    plant(2, 7777)                      # mid-context, cached
+    assert ctx[3] % 16 <= 13
+    plant(3, ctx[3] + 1)                # stale slot after the appended token: hidden
+    got = run_decode(gpu_lib, case)
+    ref = oracle_decode(case)
+    o = bf16_to_f64(got[0])
+    for i in range(3):
+        assert np.max(np.abs(o[i, h] - 10.0)) < 0.1, (i, o[i, h][:4])
+    assert np.max(np.abs(o[3, h] - 10.0)) > 4.0
+    check("decode spikes", got, ref)

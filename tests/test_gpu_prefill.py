@@ -151,18 +151,23 @@ def test_prefill_is_deterministic_and_placement_invariant(gpu_lib):
     assert np.array_equal(out1, out3) and np.array_equal(lse1, lse3)
 
 
-def test_prefill_spike_probes_mask_boundary(gpu_lib):
+@pytest.mark.parametrize("prefixes,news,probes", [
+    ([40, 77, 0], [50, 90, 33], ((0, 7), (1, 63), (2, 20))),
+    # long cached prefixes: the boundary sits past the first 64-entry table chunk, in the
+    # 65th and later key tiles, and (8191 + 32) in the last slot of a block
+    ([4096, 5000, 8191], [40, 90, 34], ((0, 0), (1, 63), (2, 32))),
+], ids=["short", "long"])
+def test_prefill_spike_probes_mask_boundary(gpu_lib, prefixes, news, probes):
     """Plant a key parallel to query (j, h) at position P + j (visible: output ~ its value)
     and at P + j + 1 (hidden: output unaffected). The tolerance alone is blind to a one-key
     mask error at long context; these probes are not."""
-    say("[prefill] spike probes")
-    prefixes, news = [40, 77, 0], [50, 90, 33]
+    say(f"[prefill] spike probes, prefixes {prefixes}")
     spec = _edge_spec("spike", 130, 8, 2, 128, 3)
     for offset in (0, 1):
         case = W.make_case(spec, prefix_override=[prefixes], new_override=[news])
         b = case.batches[0]
         probes = []
-        for i, j in ((0, 7), (1, 63), (2, 20)):
+        for i, j in probes:
             h = 5
             row = int(b.cu_new_lens[i]) + j
             qv = bf16_to_f64(b.q[row, h])
