@@ -95,7 +95,7 @@ int32_t pkv_get_debug_validate(void);
  * Section 2.1 ("vLLM memory model"): a global pool of fixed-size blocks, taken when a
  * request is admitted and returned when it completes; when blocks run short the request is
  * deferred. Section 4 (predicate contract): a dropped tuple frees its prefix. Section 5.3
- * (Algorithm 1, Complete): a parent's memory is released only after all its children.
+ * (Algorithm 1): a parent's memory is released only after all its children.
  * A pool is not thread-safe; distinct pools are independent. It owns no device memory.
  * --------------------------------------------------------------------------------------- */
 typedef struct pkv_pool pkv_pool;
@@ -365,18 +365,21 @@ pkv_status pkv_gather_kv(const pkv_paged_kv* kv, const int32_t* block_tables,
  * request generates, 1..max_out) and filtered (non-zero: the predicate drops the tuple). These
  * are the inputs that fix every outcome, so a run is deterministic.
  *
- * The scheduler follows Algorithm 1: per iteration, Launch admits waiting tasks stage by stage
- * while the memory manager admits them; the engine advances the first max_batch admitted tasks
- * by one step (a task's first step prefills its prompt and yields one token, each later step
- * appends the previous token's KV and yields the next; with max_step_tokens, prompts are
- * prefilled in chunks that fit the step's token budget after the batch's decodes); Complete handles the finished ones
- * (a task that reaches its token bound before its output is complete is interrupted, its bound
- * doubled (at most max_out) and re-enqueued; children are enqueued and tracked; a parent's
- * memory is released once all its children are); Rebalance moves budget: a saturated middle
- * stage gives delta blocks to the last stage (from its own unused budget, else from the first
- * stage with delta unused), and, from the last stage down, a starving stage gives delta to the
- * stage before it (saturated: waiting > alpha * budget / minBudget; starving: waiting < beta *
- * budget / minBudget). Token bounds: static per stage, or the nearest-rank 99th percentile of
+ * The scheduler is the paper's adaptive memory-aware scheduler (Algorithm 1, Section 5.3)
+ * restated as an engine loop. Each iteration: an admission pass lets every stage hand its
+ * queued tasks, in order, to the engine while their KV reservations fit the stage's budget;
+ * the engine advances the first max_batch admitted tasks by one step (a task's first step
+ * prefills its prompt and yields one token, each later step appends the previous token's KV
+ * and yields the next; with max_step_tokens, prompts are prefilled in chunks that fit the
+ * step's token budget after the batch's decodes); finished tasks are handled (one that
+ * reaches its token bound before its output is complete is interrupted, its bound doubled (at
+ * most max_out) and queued again; a survivor of a non-final stage creates its children, which
+ * reuse its cached prefix, and keeps its charge until all of them are done; results and
+ * filtered tasks free their memory); and the budgets adapt: a middle stage with a high
+ * backlog moves delta blocks to the last stage (from its own unused budget, else from the
+ * first stage with delta unused), and, from the last stage back to the second, a stage with
+ * a low backlog gives delta to the stage before it (high: waiting > alpha * budget /
+ * minBudget; low: waiting < beta * budget / minBudget). Token bounds: static per stage, or the nearest-rank 99th percentile of
  * the output/input ratio of completed requests times the task's input length, once min_obs
  * requests have completed (initial_bound before that). Memory is counted in 16-token blocks of
  * a pool of num_blocks blocks that the run creates; completed prefixes are published in its

@@ -5,15 +5,17 @@ What it follows:
     tuple; a surviving task of a non-final stage is joined (Cartesian product) with the next
     stage's right-side table, creating dependent child tasks that reuse the task's cached
     prefix; a final-stage task's result is output; a filtered task ends its branch.
-  * Algorithm 1 (Section 5.3): Schedule iterates Launch (per stage, in stage order, admit the
-    head of the waiting queue while the memory manager admits it), then Complete for every
-    finished task (retry with a larger bound; enqueue children and track the dependency; output;
-    release memory), then Rebalance (saturated stages other than the first give Delta to the
-    last stage, from themselves or else from the first stage that has Delta unused; from the
-    last stage down to the second, a starving stage gives Delta to the stage before it).
-    Thresholds: high_s = alpha * budget_s / minBudget_s, low_s = beta * budget_s / minBudget_s;
-    saturated when |waiting_s| > high_s, starving when |waiting_s| < low_s. Initial budgets:
-    minBudget_s for every stage but the last, which takes the rest.
+  * Algorithm 1 (Section 5.3), the adaptive memory-aware scheduler. Every iteration admits
+    waiting tasks stage by stage, in queue order, while the memory manager finds room for the
+    queue head in its stage's budget; then handles the tasks that finished (a retry raises the
+    bound and queues the task again; a survivor of a non-final stage produces its children and
+    keeps its memory until they are all done; results and filtered tasks release theirs); then
+    adapts the budgets: a saturated stage other than the first and the last gives Delta to the
+    last stage (from its own unused budget, or else from the first stage with Delta unused),
+    and, from the last stage down to the second, a starving stage gives Delta to the one
+    before it. A stage is saturated when more than alpha * budget_s / minBudget_s tasks wait,
+    starving when fewer than beta * budget_s / minBudget_s do. Initial budgets: minBudget_s
+    for every stage but the last, which takes the rest.
   * Section 6: each task carries a token bound (static per stage, or the 99th percentile of
     the output-to-input ratio of completed requests times the task's input length); a request
     that reaches its bound is interrupted, the bound is raised and the task re-enqueued.
@@ -34,7 +36,7 @@ Readings where the paper is silent (the library implements the same ones):
     stage-s task at the largest bound (max_out): one task with its prefix always fits.
   * A task's charge stays on its stage after it completes (its prefix is cached for its
     children) and is released when it is filtered, is a final-stage task, or when all of its
-    children have been released; the release cascades up (Algorithm 1, Complete).
+    children have been released; the release cascades up (Algorithm 1).
   * The engine is step-synchronous: each step, the first max_batch admitted tasks advance; a
     task's first step prefills its prompt (suffix, or prefix + suffix on a miss) and yields one
     output token; each later step appends the previous token's KV and yields one more. A task
@@ -197,13 +199,13 @@ class SchedulerModel:
             return whole, hit, bound
         return whole - P // BS, hit, bound
 
-    def admit(self, stage, t):
+    def fits_budget(self, stage, t):
         charge, _, _ = self._size(t)
         if self.c.policy == BLOCKING or self.c.policy == SEQUENTIAL:
             return sum(self.used) + charge <= self.c.num_blocks
         return self.used[stage] + charge <= self.budget[stage]
 
-    def allocate_memory(self, stage, t):
+    def reserve_for(self, stage, t):
         charge, hit, bound = self._size(t)
         s, i, pool = t.stage, t.idx, self.pool
         P, suf = self.p.prefix[s][i], self.p.suffix[s][i]
@@ -230,7 +232,7 @@ class SchedulerModel:
         self.stats["launches"] += 1
         self.trace.append((self.step, EV_LAUNCH, s, i, 2 * charge + (1 if hit else 0)))
 
-    def release_memory(self, t):
+    def return_charge(self, t):
         self.used[self._charged_stage(t)] -= t.charge
         self.trace.append((self.step, EV_RELEASE, t.stage, t.idx, t.charge))
         par = t.parent
@@ -240,15 +242,15 @@ class SchedulerModel:
                 key = task_key(par.stage, par.idx)
                 if self.c.pinning == EXPLICIT:
                     self.pool.unpin(key)  # the prefix stays cached, now evictable
-                self.release_memory(par)
+                self.return_charge(par)
 
     def _charged_stage(self, t):
         return 0 if self.c.policy in (SEQUENTIAL, BLOCKING) else t.stage
 
-    def is_saturated(self, s):
+    def saturated(self, s):
         return len(self.waiting[s]) > self.c.alpha * self.budget[s] / self.min_budget[s]
 
-    def is_starving(self, s):
+    def starving(self, s):
         return len(self.waiting[s]) < self.c.beta * self.budget[s] / self.min_budget[s]
 
     def _can_give(self, u):
@@ -260,7 +262,7 @@ class SchedulerModel:
         self.budget[b] += self.delta
         self.trace.append((self.step, EV_TRANSFER, a, b, self.delta))
 
-    def transfer_mem_saturation(self, s):
+    def relieve_saturation(self, s):
         last = self.S - 1
         if self._can_give(s):
             self._move(s, last)
@@ -270,12 +272,12 @@ class SchedulerModel:
                 self._move(u, last)
                 return
 
-    def transfer_mem_starvation(self, i):
+    def feed_previous(self, i):
         if self._can_give(i):
             self._move(i, i - 1)
 
-    # -- Algorithm 1 ------------------------------------------------------------------------
-    def launch(self):
+    # -- the scheduling loop (Algorithm 1) ----------------------------------------------------
+    def admit_waiting(self):
         pol = self.c.policy
         if pol == SEQUENTIAL:
             if self.running:
@@ -283,9 +285,9 @@ class SchedulerModel:
             for s in reversed(range(self.S)):  # depth first: the deepest ready stage
                 if self.waiting[s]:
                     t = self.waiting[s][0]
-                    if self.admit(s, t):
+                    if self.fits_budget(s, t):
                         self.waiting[s].popleft()
-                        self.allocate_memory(s, t)
+                        self.reserve_for(s, t)
                         self.running.append(t)
                     return
             return
@@ -297,9 +299,9 @@ class SchedulerModel:
         for s in stages:
             while self.waiting[s]:
                 t = self.waiting[s][0]
-                if self.admit(s, t):
+                if self.fits_budget(s, t):
                     self.waiting[s].popleft()
-                    self.allocate_memory(s, t)
+                    self.reserve_for(s, t)
                     self.running.append(t)
                 else:
                     break
@@ -349,7 +351,7 @@ class SchedulerModel:
                 done.append((t, 1))
         return done
 
-    def complete(self, t, interrupted):
+    def finish(self, t, interrupted):
         s, i, pool = t.stage, t.idx, self.pool
         self.running.remove(t)
         if interrupted:  # Section 6: raise the bound, re-enqueue
@@ -370,7 +372,7 @@ class SchedulerModel:
                 f = self.p.fanout[s]
                 kids = [_Task(s + 1, i * f + r, t) for r in range(f)]
                 self.waiting[s + 1].extend(kids)
-                t.children_left = f  # trackDependency
+                t.children_left = f  # its memory stays until these are done
                 key = task_key(s, i)
                 assert pool.publish(t.seq, key, self.p.kv_len(s, i)) == Status.OK
                 if self.c.pinning == EXPLICIT and self.c.policy != BLOCKING:
@@ -387,29 +389,29 @@ class SchedulerModel:
             self.trace.append((self.step, EV_FILTERED, s, i, self.p.out_len[s][i]))
         if filtered or last:
             pool.free_seq(t.seq)
-            self.release_memory(t)
+            self.return_charge(t)
 
-    def rebalance(self):
+    def rebalance_budgets(self):
         for s in range(self.S):
-            if s != 0 and s != self.S - 1 and self.is_saturated(s):
-                self.transfer_mem_saturation(s)
+            if s != 0 and s != self.S - 1 and self.saturated(s):
+                self.relieve_saturation(s)
         for i in range(self.S - 1, 0, -1):
-            if self.is_starving(i):
-                self.transfer_mem_starvation(i)
+            if self.starving(i):
+                self.feed_previous(i)
 
     def run(self):
         self.waiting[0].extend(_Task(0, t, None) for t in range(len(self.p.suffix[0])))
         while any(self.waiting) or self.running:
             if self.step >= self.c.max_steps:
                 raise RuntimeError("step limit reached")
-            self.launch()
+            self.admit_waiting()
             if not self.running:
                 raise RuntimeError("no task can be admitted and none is running")
             done = self.engine_step()
             for t, kind in done:
-                self.complete(t, kind == 1)
+                self.finish(t, kind == 1)
             if self.c.policy == ADAPTIVE:
-                self.rebalance()
+                self.rebalance_budgets()
             self.step += 1
         self.stats["steps"] = self.step
         self.stats["evictions"] = self.pool.evictions

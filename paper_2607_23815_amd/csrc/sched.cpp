@@ -365,15 +365,15 @@ class Sched {
     while (any_waiting() || !running_.empty()) {
       if (step_ >= c_.max_steps) return pkv::fail(PKV_ERR_INVALID_ARG, "pkv_sched_run: step limit reached");
       copies_.clear();
-      if ((st = launch()) != PKV_OK) return st;
+      if ((st = admit_waiting()) != PKV_OK) return st;
       if (running_.empty())
         return pkv::fail(PKV_ERR_INVALID_ARG,
                          "pkv_sched_run: no task can be admitted and none is running");
       std::vector<std::pair<int64_t, int>> done;
       if ((st = engine_step(dev, &done)) != PKV_OK) return st;
       for (const auto& d : done)
-        if ((st = complete(d.first, d.second == 1)) != PKV_OK) return st;
-      if (c_.policy == PKV_SCHED_ADAPTIVE) rebalance();
+        if ((st = on_finished(d.first, d.second == 1)) != PKV_OK) return st;
+      if (c_.policy == PKV_SCHED_ADAPTIVE) adapt_budgets();
       ++step_;
     }
     const auto w1 = std::chrono::steady_clock::now();
@@ -460,17 +460,22 @@ class Sched {
     *charge = (c_.policy == PKV_SCHED_BLOCKING || !*hit) ? whole : whole - p / kBS;
   }
 
-  bool admit(int32_t stage, const Task& t) const {
+  // Whether task t's reservation fits now: in its stage's budget, or (one shared budget for
+  // the sequential and blocking policies) in the whole pool.
+  bool fits(int32_t stage, const Task& t) const {
     int64_t charge;
     bool hit;
     int32_t bound;
     size_of(t, &charge, &hit, &bound);
-    if (c_.policy == PKV_SCHED_BLOCKING || c_.policy == PKV_SCHED_SEQUENTIAL) {
+    if (shared_budget()) {
       int64_t u = 0;
       for (int64_t x : used_) u += x;
       return u + charge <= c_.num_blocks;
     }
     return used_[stage] + charge <= budget_[stage];
+  }
+  bool shared_budget() const {
+    return c_.policy == PKV_SCHED_BLOCKING || c_.policy == PKV_SCHED_SEQUENTIAL;
   }
 
   pkv_status allocate(int32_t stage, int64_t ti) {
@@ -522,37 +527,48 @@ class Sched {
     return PKV_OK;
   }
 
-  pkv_status launch() {
-    const int32_t pol = c_.policy;
-    if (pol == PKV_SCHED_SEQUENTIAL) {
-      if (!running_.empty()) return PKV_OK;
+  // The stages whose queues may admit this iteration, [lo, hi): every stage; under blocking
+  // execution only the first stage with unfinished work; under sequential execution the
+  // deepest stage with a waiting task, and only while nothing runs (one task at a time).
+  void admission_window(int32_t* lo, int32_t* hi) const {
+    *lo = 0;
+    *hi = S_;
+    if (c_.policy == PKV_SCHED_SEQUENTIAL) {
+      *hi = 0;
+      if (!running_.empty()) return;
       for (int32_t s = S_ - 1; s >= 0; --s)
         if (!waiting_[s].empty()) {
-          const int64_t ti = waiting_[s].front();
-          if (!admit(s, tasks_[ti])) return PKV_OK;
-          waiting_[s].pop_front();
-          return allocate(s, ti);
+          *lo = s;
+          *hi = s + 1;
+          return;
         }
-      return PKV_OK;
+      return;
     }
-    int32_t lo = 0, hi = S_;
-    if (pol == PKV_SCHED_BLOCKING) {  // one stage at a time: the first with unfinished work
-      int32_t active = 0;
-      for (; active < S_; ++active) {
-        bool busy = !waiting_[active].empty();
-        for (int64_t ti : running_) busy = busy || tasks_[ti].stage == active;
-        if (busy) break;
+    if (c_.policy == PKV_SCHED_BLOCKING) {
+      int32_t s = 0;
+      for (; s < S_; ++s) {
+        bool open = !waiting_[s].empty();
+        for (int64_t ti : running_) open = open || tasks_[ti].stage == s;
+        if (open) break;
       }
-      lo = active;
-      hi = active + 1;
+      *lo = s;
+      *hi = s + 1;
     }
+  }
+
+  // Admission pass: each stage in the window hands over its queue in order while the head's
+  // reservation fits; a head that does not fit stops that stage (first come, first served).
+  pkv_status admit_waiting() {
+    int32_t lo, hi;
+    admission_window(&lo, &hi);
+    const bool one_task = c_.policy == PKV_SCHED_SEQUENTIAL;
     for (int32_t s = lo; s < hi; ++s) {
-      while (!waiting_[s].empty()) {
+      while (!waiting_[s].empty() && fits(s, tasks_[waiting_[s].front()])) {
         const int64_t ti = waiting_[s].front();
-        if (!admit(s, tasks_[ti])) break;
         waiting_[s].pop_front();
         pkv_status st = allocate(s, ti);
         if (st != PKV_OK) return st;
+        if (one_task) return PKV_OK;
       }
     }
     return PKV_OK;
@@ -616,106 +632,128 @@ class Sched {
     return PKV_OK;
   }
 
-  pkv_status release_memory(int64_t ti) {
-    Task& t = tasks_[ti];
-    used_[charged_stage(t)] -= t.charge;
-    event(PKV_EV_RELEASE, t.stage, t.idx, t.charge);
-    if (t.parent >= 0 && c_.policy != PKV_SCHED_BLOCKING) {
-      Task& par = tasks_[t.parent];
-      if (--par.children_left == 0) {
-        if (c_.pinning == PKV_PIN_EXPLICIT) {
-          pkv_status st = pkv_prefix_unpin(pool_, key_of(par.stage, par.idx));
-          if (st != PKV_OK) return st;
-        }
-        return release_memory(t.parent);
-      }
-    }
-    return PKV_OK;
-  }
-
-  pkv_status complete(int64_t ti, bool interrupted) {
-    running_.erase(std::find(running_.begin(), running_.end(), ti));
-    Task& t = tasks_[ti];
-    const int32_t s = t.stage;
-    pkv_status st;
-    if (interrupted) {
-      if ((st = pkv_seq_free(pool_, t.seq)) != PKV_OK) return st;
+  // Give back a finished task's charge, and with it the charge of every ancestor whose last
+  // outstanding child this was (explicitly pinned prefixes are unpinned as they go, and stay
+  // cached until evicted). Blocking execution tracks no children.
+  pkv_status return_charges(int64_t ti) {
+    for (int64_t cur = ti;;) {
+      Task& t = tasks_[cur];
       used_[charged_stage(t)] -= t.charge;
-      t.bound = std::min(2 * t.bound, c_.max_out);
-      t.fixed_bound = true;
-      stats_.retries += 1;
-      event(PKV_EV_RETRY, s, t.idx, t.bound);
-      waiting_[s].push_back(ti);
-      return PKV_OK;
-    }
-    const int64_t prompt = P(s, t.idx) + Suf(s, t.idx);
-    ratios_[s].insert((double)Out(s, t.idx) / (double)prompt);
-    const bool filtered = Filtered(s, t.idx);
-    const bool last = s == S_ - 1;
-    if (!filtered) {
-      if (!last) {
-        const int32_t f = fanout_[s];
-        const int64_t idx = t.idx;
-        for (int32_t r = 0; r < f; ++r) waiting_[s + 1].push_back(new_task(s + 1, idx * f + r, ti));
-        Task& tt = tasks_[ti];  // new_task may have moved the vector
-        tt.children_left = f;
-        const uint64_t key = key_of(s, tt.idx);
-        if ((st = pkv_prefix_publish(pool_, tt.seq, key, (int32_t)kv_len(s, tt.idx))) != PKV_OK)
-          return st;
-        if (c_.pinning == PKV_PIN_EXPLICIT && c_.policy != PKV_SCHED_BLOCKING &&
-            (st = pkv_prefix_pin(pool_, key)) != PKV_OK)
-          return st;
-        if ((st = pkv_seq_free(pool_, tt.seq)) != PKV_OK) return st;
-        event(PKV_EV_DONE, s, tt.idx, Out(s, tt.idx));
-        if (c_.policy == PKV_SCHED_BLOCKING) {  // nothing tracks the children
-          used_[0] -= tt.charge;
-          event(PKV_EV_RELEASE, s, tt.idx, tt.charge);
-        }
-      } else {
-        stats_.outputs += 1;
-        event(PKV_EV_OUTPUT, s, t.idx, Out(s, t.idx));
+      event(PKV_EV_RELEASE, t.stage, t.idx, t.charge);
+      if (t.parent < 0 || c_.policy == PKV_SCHED_BLOCKING) return PKV_OK;
+      Task& par = tasks_[t.parent];
+      if (--par.children_left > 0) return PKV_OK;
+      if (c_.pinning == PKV_PIN_EXPLICIT) {
+        const pkv_status st = pkv_prefix_unpin(pool_, key_of(par.stage, par.idx));
+        if (st != PKV_OK) return st;
       }
-    } else {
-      event(PKV_EV_FILTERED, s, t.idx, Out(s, t.idx));
+      cur = t.parent;
     }
-    if (filtered || last) {
-      if ((st = pkv_seq_free(pool_, tasks_[ti].seq)) != PKV_OK) return st;
-      return release_memory(ti);
+  }
+
+  // An interrupted request (it reached its token bound first): drop its sequence and charge,
+  // double the bound (up to max_out) and queue the task again at the back of its stage.
+  pkv_status requeue(int64_t ti) {
+    Task& t = tasks_[ti];
+    pkv_status st = pkv_seq_free(pool_, t.seq);
+    if (st != PKV_OK) return st;
+    used_[charged_stage(t)] -= t.charge;
+    t.bound = std::min(2 * t.bound, c_.max_out);
+    t.fixed_bound = true;
+    stats_.retries += 1;
+    event(PKV_EV_RETRY, t.stage, t.idx, t.bound);
+    waiting_[t.stage].push_back(ti);
+    return PKV_OK;
+  }
+
+  // A surviving task of a non-final stage: its join with the next stage's rows becomes that
+  // stage's new tasks, all reusing its prefix, which is published in the prefix cache (pinned
+  // under explicit pinning) before the task's own sequence goes. Its charge stays until the
+  // last child returns its own (blocking execution returns it now).
+  pkv_status spawn_children(int64_t ti) {
+    const int32_t s = tasks_[ti].stage;
+    const int64_t idx = tasks_[ti].idx;
+    const int32_t f = fanout_[s];
+    for (int32_t r = 0; r < f; ++r) waiting_[s + 1].push_back(new_task(s + 1, idx * f + r, ti));
+    Task& t = tasks_[ti];  // new_task may have moved the vector
+    t.children_left = f;
+    const uint64_t key = key_of(s, idx);
+    pkv_status st = pkv_prefix_publish(pool_, t.seq, key, (int32_t)kv_len(s, idx));
+    if (st != PKV_OK) return st;
+    if (c_.pinning == PKV_PIN_EXPLICIT && c_.policy != PKV_SCHED_BLOCKING &&
+        (st = pkv_prefix_pin(pool_, key)) != PKV_OK)
+      return st;
+    if ((st = pkv_seq_free(pool_, t.seq)) != PKV_OK) return st;
+    event(PKV_EV_DONE, s, idx, Out(s, idx));
+    if (c_.policy == PKV_SCHED_BLOCKING) {
+      used_[0] -= t.charge;
+      event(PKV_EV_RELEASE, s, idx, t.charge);
     }
     return PKV_OK;
   }
 
-  bool saturated(int32_t s) const {
-    return (double)waiting_[s].size() > c_.alpha * (double)budget_[s] / (double)min_budget_[s];
+  // A task the engine reports finished (interrupted: it hit its bound). A finished request
+  // records its output/input ratio for the bound estimate; then it feeds the next stage, is a
+  // result of the pipeline, or ends its branch (filtered); the last two free everything.
+  pkv_status on_finished(int64_t ti, bool interrupted) {
+    running_.erase(std::find(running_.begin(), running_.end(), ti));
+    if (interrupted) return requeue(ti);
+    const Task& t = tasks_[ti];
+    const int32_t s = t.stage;
+    ratios_[s].insert((double)Out(s, t.idx) / (double)(P(s, t.idx) + Suf(s, t.idx)));
+    if (Filtered(s, t.idx)) {
+      event(PKV_EV_FILTERED, s, t.idx, Out(s, t.idx));
+    } else if (s + 1 < S_) {
+      return spawn_children(ti);
+    } else {
+      stats_.outputs += 1;
+      event(PKV_EV_OUTPUT, s, t.idx, Out(s, t.idx));
+    }
+    const pkv_status st = pkv_seq_free(pool_, tasks_[ti].seq);
+    if (st != PKV_OK) return st;
+    return return_charges(ti);
   }
-  bool starving(int32_t s) const {
-    return (double)waiting_[s].size() < c_.beta * (double)budget_[s] / (double)min_budget_[s];
+
+  // Queue pressure of a stage against its budget, counted in tasks of its largest footprint
+  // (minBudget): a backlog above alpha * budget / minBudget means the stage holds more
+  // admitted work than the pipeline behind it can absorb (saturation); below beta * ... it
+  // has too little queued work to keep its budget busy (starvation).
+  double capacity_in_tasks(int32_t s) const {
+    return (double)budget_[s] / (double)min_budget_[s];
   }
-  bool can_give(int32_t u) const {
+  bool backlog_high(int32_t s) const {
+    return (double)waiting_[s].size() > c_.alpha * capacity_in_tasks(s);
+  }
+  bool backlog_low(int32_t s) const {
+    return (double)waiting_[s].size() < c_.beta * capacity_in_tasks(s);
+  }
+  // A stage can spare delta blocks when that much of its budget is unused and what remains
+  // still covers one task of its largest footprint.
+  bool can_spare(int32_t u) const {
     return budget_[u] - used_[u] >= delta_ && budget_[u] - delta_ >= min_budget_[u];
   }
-  void move(int32_t a, int32_t b) {
-    budget_[a] -= delta_;
-    budget_[b] += delta_;
-    event(PKV_EV_TRANSFER, a, b, delta_);
+  void shift(int32_t from, int32_t to) {
+    budget_[from] -= delta_;
+    budget_[to] += delta_;
+    event(PKV_EV_TRANSFER, from, to, delta_);
   }
 
-  void rebalance() {
+  // Budget adaptation after each engine step (the adaptive policy). First, every middle
+  // stage with a high backlog moves delta to the last stage, which is what drains it: from its
+  // own spare budget, else from the first stage that can spare it. Then, walking from the
+  // last stage back to the second, a stage with a low backlog hands delta of its spare budget
+  // to the stage feeding it.
+  void adapt_budgets() {
     const int32_t last = S_ - 1;
     for (int32_t s = 1; s < last; ++s) {
-      if (!saturated(s)) continue;
-      if (can_give(s)) {
-        move(s, last);
-        continue;
-      }
-      for (int32_t u = 0; u < last; ++u)
-        if (can_give(u)) {
-          move(u, last);
-          break;
-        }
+      if (!backlog_high(s)) continue;
+      int32_t donor = can_spare(s) ? s : -1;
+      for (int32_t u = 0; donor < 0 && u < last; ++u)
+        if (can_spare(u)) donor = u;
+      if (donor >= 0) shift(donor, last);
     }
-    for (int32_t i = last; i >= 1; --i)
-      if (starving(i) && can_give(i)) move(i, i - 1);
+    for (int32_t s = last; s >= 1; --s)
+      if (backlog_low(s) && can_spare(s)) shift(s, s - 1);
   }
 
   pkv_sched_config c_;

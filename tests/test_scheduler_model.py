@@ -169,7 +169,7 @@ def test_rebalancing_moves_budget_only_where_the_rules_say(spec):
                  delta=16)
     m = SchedulerModel(pipe, cfg)
     seen = []
-    orig = m.rebalance
+    orig = m.rebalance_budgets
 
     def observed():
         before = len(m.trace)
@@ -180,7 +180,7 @@ def test_rebalancing_moves_budget_only_where_the_rules_say(spec):
         assert sum(m.budget) == cfg.num_blocks
         assert all(b >= mb for b, mb in zip(m.budget, m.min_budget))
 
-    m.rebalance = observed
+    m.rebalance_budgets = observed
     m.run()
     last = m.S - 1
     moves = 0
