@@ -243,7 +243,7 @@ def test_prefixes_are_pinned_exactly_while_children_need_them(pinning):
     m = SchedulerModel(pipe, Config(ADAPTIVE, 2500, max_out=64, initial_bound=[8] * pipe.S,
                                     max_batch=16, pinning=pinning))
     tasks = {}
-    orig = m.complete
+    orig = m.finish
 
     def complete(t, interrupted):
         tasks[(t.stage, t.idx)] = t
@@ -255,7 +255,7 @@ def test_prefixes_are_pinned_exactly_while_children_need_them(pinning):
             elif e is not None:
                 assert e.pins == 0
 
-    m.complete = complete
+    m.finish = complete
     m.run()
     assert tasks
 
