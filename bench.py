@@ -533,6 +533,35 @@ def secondary(args, lib, torch, flush):
                       "prefill_frac_mfma": flops / tp / 1e12 / PEAK_BF16_TFLOPS,
                       "tuples_per_s": b.n_seqs / med(step)}
     del wl, pk, pv
+
+    # a batch too small to fill the chip (4 tuples of 24-32k cached tokens, short suffixes):
+    # the prefill without a workspace (no key split) and with one (key split + merge)
+    spec = W.LONG_PREFIX_FEW_TUPLES
+    wl = Workload(spec, lib, torch)
+    b, _ = wl.batches[0]
+    dv = wl.dev[0]
+    pk, pv = wl.case.pool_k, wl.case.pool_v
+    lib.pkv_kv_append(pk, pv, b.k_new, b.v_new, dv["tables"], dv["cached"], dv["cu"],
+                      dv["max_new"])
+    o = torch.empty((b.total_new, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
+    nb = lib.pkv_prefill_workspace_bytes(b.n_seqs, b.total_new, wl.hq, wl.hkv, wl.d,
+                                         dv["max_new"], dv["max_total"])
+    ws = lib.alloc_workspace(nb)
+    fns = [lambda: lib.pkv_prefill_attention(pk, pv, b.q, dv["tables"], dv["cached"], dv["cu"],
+                                             dv["max_new"], dv["max_total"], wl.scale, o),
+           lambda: lib.pkv_prefill_attention(pk, pv, b.q, dv["tables"], dv["cached"], dv["cu"],
+                                             dv["max_new"], dv["max_total"], wl.scale, o,
+                                             workspace=ws)]
+    _, step, per = time_steps(torch, stream, fns, steps, warm, flush)
+    flops = prefill_flops(b.prefix_lens, b.new_lens, wl.hq, wl.d)
+    tu, tsp = med(per[:, 0]), med(per[:, 1])
+    out[spec.name] = {"unsplit_ms": dist(per[:, 0]), "unsplit_TFLOP_s": flops / tu / 1e12,
+                      "split_ms": dist(per[:, 1]), "split_TFLOP_s": flops / tsp / 1e12,
+                      "split_frac_mfma": flops / tsp / 1e12 / PEAK_BF16_TFLOPS,
+                      "speedup": tu / tsp, "workspace_MB": nb / 1e6,
+                      "note": "prefill key split (workspace given) against the launch without "
+                              "a workspace, same inputs; split time includes the merge kernel"}
+    del wl, pk, pv, ws
     torch.cuda.empty_cache()
     return out
 
@@ -854,6 +883,11 @@ def summary(res):
         log(f"[summary] long docs: prefill {s['prefill_ms']['median']:.3f} ms "
             f"({s['prefill_TFLOP_s']:.0f} TF, {100 * s['prefill_frac_mfma']:.1f}%), append "
             f"{s['append_ms']['median'] * 1e3:.1f} us ({100 * s['append_frac_hbm']:.1f}%)")
+    s = sec.get("long_prefix_few_tuples")
+    if s:
+        log(f"[summary] long prefix, few tuples: prefill {s['unsplit_ms']['median']:.3f} ms "
+            f"unsplit, {s['split_ms']['median']:.3f} ms with the key split "
+            f"({s['split_TFLOP_s']:.0f} TF, {s['speedup']:.2f}x)")
     r = sec.get("reuse_vs_recompute")
     if r:
         log("[summary] reuse vs recompute: " + ", ".join(

@@ -42,8 +42,8 @@
  *     blocks are handed out, not device pointers or a seed; the caller allocates the K/V
  *     tensors); device calls take host maxima (max_new_len, max_total_len, max_seq_len,
  *     max_len) that size the launch without a device-to-host read; the pool layout below is
- *     chunk-major K and dim-major V rather than row-major slabs; prefill needs no workspace
- *     (pkv_prefill_workspace_bytes returns 0 and keeps its arguments for future kernels).
+ *     chunk-major K and dim-major V rather than row-major slabs; the prefill's workspace is
+ *     optional (it enables the key split of batches too small to fill the chip).
  *   - bf16 is IEEE binary16 "brain float" (1 sign, 8 exponent, 7 mantissa bits), stored as
  *     16-bit words.
  *
@@ -265,13 +265,27 @@ pkv_status pkv_kv_append(const pkv_paged_kv* kv, const void* k_new, const void* 
  * attention over the whole P_i + N_i tokens. q, out: bf16 [total_new][num_q_heads][head_dim];
  * lse: float [total_new][num_q_heads] or NULL. bf16 inputs, fp32 accumulation, bf16 output
  * (round to nearest even). max_new_len (host) >= every N_i; max_total_len (host) >= every
- * P_i + N_i. workspace may be NULL when pkv_prefill_workspace_bytes returns 0. */
+ * P_i + N_i.
+ * Key split (optional): a batch whose work items -- sequences x kv heads x tiles of 128
+ * query columns, a column being one (new token, query head of the kv group) -- number
+ * fewer than 1024 cannot keep the chip busy; when its keys are long (max_total_len >= 2048)
+ * and the caller passes a workspace of at least pkv_prefill_workspace_bytes (16-byte
+ * aligned, caller-owned, not read back), every item's keys are cut at multiples of a split
+ * size (a multiple of 1024 keys chosen from the host arguments) into parts run as separate
+ * work items; a row whose keys end in the first part is finished there, the others are
+ * merged from their parts' partial results by log-sum-exp weights in a second kernel. The
+ * cut points depend on key positions and host arguments only, so results are
+ * deterministic. With workspace NULL (or when the size is 0) the launch does not split; a
+ * non-NULL workspace smaller than the size is refused. Calls sharing a workspace must not
+ * overlap. */
 pkv_status pkv_prefill_attention(const pkv_paged_kv* kv, const void* q, int32_t num_q_heads,
                                  const int32_t* block_tables, int32_t max_blocks,
                                  const int32_t* cached_lens, const int32_t* cu_new_lens,
                                  int32_t num_seqs, int32_t total_new, int32_t max_new_len,
                                  int32_t max_total_len, float scale, void* out, float* lse,
                                  void* workspace, size_t workspace_bytes, void* stream);
+/* Workspace that enables the prefill's key split: total_new x num_q_heads x splits x
+ * (head_dim + 2) floats when the batch splits, else 0. */
 size_t pkv_prefill_workspace_bytes(int32_t num_seqs, int32_t total_new, int32_t num_q_heads,
                                    int32_t num_kv_heads, int32_t head_dim,
                                    int32_t max_new_len, int32_t max_total_len);
@@ -324,8 +338,8 @@ pkv_status pkv_copy_blocks(const pkv_paged_kv* kv, const int32_t* pairs, int32_t
 
 /* Mixed prefill + decode (the mixed batch of a serving step: downstream operators
  * prefilling their suffixes while other tuples decode). Identical results, bit for bit, to
- * pkv_prefill_attention on the prefill arguments (q .. lse, as there; no workspace) followed
- * by pkv_decode_attention on the decode arguments (dq .. d_lse, with workspace and
+ * pkv_prefill_attention on the prefill arguments (q .. lse, as there, without a workspace:
+ * the fused launch does not split keys) followed by pkv_decode_attention on the decode arguments (dq .. d_lse, with workspace and
  * workspace_bytes as there), with the same num_q_heads and scale; either batch may be empty
  * (zero sequences or zero new tokens). Both read the same pool, so the new tokens of both
  * batches must have been appended before the call. One fused kernel runs prefill workgroups

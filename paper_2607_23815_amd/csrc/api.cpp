@@ -146,10 +146,14 @@ pkv_status check_prefill(const KvView& view, const char* fn, const void* q, int3
   if (!(scale > 0.f)) return fail(PKV_ERR_INVALID_ARG, f + ": scale <= 0");
   if (num_seqs > kMaxGridZ)
     return fail(PKV_ERR_INVALID_ARG, f + ": more than 65535 sequences");
-  const size_t need = pkv_prefill_workspace_bytes(num_seqs, total_new, num_q_heads, view.hkv,
-                                                  view.head_dim, max_new_len, max_total_len);
-  if (need > 0 && (workspace == nullptr || workspace_bytes < need))
-    return fail(PKV_ERR_INVALID_ARG, f + ": workspace too small");
+  // A workspace enables the key split of batches too small to fill the chip; without one
+  // (NULL) the launch does not split. One that is given must hold what the split needs.
+  const size_t need = prefill_workspace_bytes(num_seqs, total_new, num_q_heads, view.hkv,
+                                              view.head_dim, max_new_len, max_total_len);
+  if (need > 0 && workspace != nullptr && (workspace_bytes < need || !aligned16(workspace)))
+    return fail(PKV_ERR_INVALID_ARG,
+                f + ": workspace too small or not 16-byte aligned (see "
+                    "pkv_prefill_workspace_bytes; NULL runs without the key split)");
   return ok();
 }
 
@@ -254,9 +258,12 @@ pkv_status pkv_kv_append(const pkv_paged_kv* kv, const void* k_new, const void* 
 size_t pkv_prefill_workspace_bytes(int32_t num_seqs, int32_t total_new, int32_t num_q_heads,
                                    int32_t num_kv_heads, int32_t head_dim, int32_t max_new_len,
                                    int32_t max_total_len) {
-  (void)num_seqs; (void)total_new; (void)num_q_heads; (void)num_kv_heads; (void)head_dim;
-  (void)max_new_len; (void)max_total_len;
-  return 0;
+  if (num_seqs <= 0 || total_new <= 0 || num_q_heads <= 0 || num_kv_heads <= 0 ||
+      head_dim <= 0 || max_new_len <= 0 || max_total_len <= 0 ||
+      num_q_heads % num_kv_heads != 0)
+    return 0;
+  return prefill_workspace_bytes(num_seqs, total_new, num_q_heads, num_kv_heads, head_dim,
+                                 max_new_len, max_total_len);
 }
 
 pkv_status pkv_prefill_attention(const pkv_paged_kv* kv, const void* q, int32_t num_q_heads,
@@ -279,9 +286,13 @@ pkv_status pkv_prefill_attention(const pkv_paged_kv* kv, const void* q, int32_t 
                              cu_new_lens, num_seqs, total_new, max_new_len, max_total_len);
     if ((st = check_metadata(fn, &c, 1, static_cast<hipStream_t>(stream))) != PKV_OK) return st;
   }
+  const bool split = workspace != nullptr &&
+                     prefill_workspace_bytes(num_seqs, total_new, num_q_heads, view.hkv,
+                                             view.head_dim, max_new_len, max_total_len) > 0;
   return launched(launch_prefill(view, static_cast<const uint16_t*>(q), num_q_heads,
                                  block_tables, max_blocks, cached_lens, cu_new_lens, num_seqs,
-                                 max_new_len, scale, static_cast<uint16_t*>(out), lse,
+                                 total_new, max_new_len, max_total_len, scale,
+                                 static_cast<uint16_t*>(out), lse, split ? workspace : nullptr,
                                  static_cast<hipStream_t>(stream)),
                   fn);
 }
@@ -384,7 +395,8 @@ pkv_status pkv_mixed_attention(const pkv_paged_kv* kv, int32_t num_q_heads, floa
   if (no_decode)
     return launched(launch_prefill(view, static_cast<const uint16_t*>(q), num_q_heads,
                                    block_tables, max_blocks, cached_lens, cu_new_lens, num_seqs,
-                                   max_new_len, scale, static_cast<uint16_t*>(out), lse, s),
+                                   total_new, max_new_len, max_total_len, scale,
+                                   static_cast<uint16_t*>(out), lse, nullptr, s),
                     fn);
   if (no_prefill)
     return launched(launch_decode(view, static_cast<const uint16_t*>(dq), num_q_heads,

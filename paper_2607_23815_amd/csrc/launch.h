@@ -29,11 +29,27 @@ hipError_t launch_gather_kv(const KvView& kv, const int32_t* block_tables, int32
 hipError_t launch_copy_blocks(const KvView& kv, const int32_t* pairs, int32_t num_pairs,
                               hipStream_t stream);
 
+// Prefill key split: a batch whose work items cannot fill the chip (few sequences, few new
+// tokens) and whose keys are long has each item's keys cut at multiples of split_keys (a
+// multiple of 1024) into nsplit parts, run as separate work items and merged; otherwise
+// split_keys = 0 and nsplit = 1. The plan depends on the host arguments only.
+struct PrefillSplit {
+  int32_t split_keys;
+  int32_t nsplit;
+};
+PrefillSplit prefill_split_plan(int32_t num_seqs, int32_t hq, int32_t hkv, int32_t max_new_len,
+                                int32_t max_total_len);
+// Workspace of a split launch (0 without a split): fp32 partial outputs
+// [total_new][hq][nsplit][head_dim], then their (maximum, weight sum) pairs.
+size_t prefill_workspace_bytes(int32_t num_seqs, int32_t total_new, int32_t hq, int32_t hkv,
+                               int32_t head_dim, int32_t max_new_len, int32_t max_total_len);
+// With workspace == nullptr the launch does not split.
 hipError_t launch_prefill(const KvView& kv, const uint16_t* q, int32_t hq,
                           const int32_t* block_tables, int32_t max_blocks,
                           const int32_t* cached_lens, const int32_t* cu_new_lens,
-                          int32_t num_seqs, int32_t max_new_len, float scale, uint16_t* out,
-                          float* lse, hipStream_t stream);
+                          int32_t num_seqs, int32_t total_new, int32_t max_new_len,
+                          int32_t max_total_len, float scale, uint16_t* out, float* lse,
+                          void* workspace, hipStream_t stream);
 
 // Decode: keys are cut into splits of `split_keys` (a multiple of 32) keys.
 int32_t decode_split_keys(int32_t num_seqs, int32_t hkv, int32_t max_seq_len);

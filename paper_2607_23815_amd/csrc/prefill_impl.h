@@ -27,6 +27,12 @@
 //      consecutive slots, i.e. one 16-byte chunk of the dim-major V slab.
 //   5. The normalised output rows leave through LDS (the K buffers, free after the last
 //      step), so that each 16-byte store covers whole rows.
+// A key split (only for batches too small to fill the chip, see prefill_split_plan) cuts
+// an item's keys at multiples of split_keys: split s covers the key tiles of
+// [s * split_keys, (s + 1) * split_keys). A row whose keys all fall in split 0 is finished
+// there; any other row leaves one partial result (unnormalised output, running maximum and
+// weight sum) per split it reaches, merged afterwards by their log-sum-exp weights. The cut
+// points depend on key positions only, so results are deterministic.
 // Masking is by selection (scores to -inf), applied only to tiles that reach past some
 // column's last visible key; V slots past the sequence end are zeroed in LDS before the last
 // tile's value product, so stale bits (NaN included) never meet a zero weight inside the
@@ -145,7 +151,9 @@ __device__ __forceinline__ void prefill_item(
     int32_t max_blocks, int32_t hq, int32_t hkv, int32_t num_blocks, float scale_log2,
     uint16_t* __restrict__ out, float* __restrict__ lse, const int i, const int kvh,
     const int qt, const int p, const int row0, const int n, const int32_t t_first,
-    const int32_t t_lane, PrefillSmem<D>& sm) {
+    const int32_t t_lane, PrefillSmem<D>& sm, const int split_keys = 0, const int split = 0,
+    const int nsplit = 1, float* __restrict__ ws_o = nullptr,
+    float* __restrict__ ws_ml = nullptr) {
   constexpr int SLAB = D * kBlockSize;
   constexpr int UNITS = SLAB / 8;        // 16-byte units per block slab
   constexpr int LPT = 4 * UNITS / kThreads;  // 16-byte units per thread per tile (K or V)
@@ -173,6 +181,12 @@ __device__ __forceinline__ void prefill_item(
   const int jmax = min(n - 1, (col0 + kCols - 1) / g);
   const int nkeys = p + jmax + 1;
   const int ntiles = (nkeys + kKeys - 1) / kKeys;
+  // this item's key tiles [kt0, kt_end): all of them, or one split (split_keys is a multiple
+  // of 1024 keys, so a split starts at a table chunk and on an even tile)
+  const int kt0 = split_keys > 0 ? split * (split_keys / kKeys) : 0;
+  const int kt_end = split_keys > 0 ? min(ntiles, kt0 + split_keys / kKeys) : ntiles;
+  if (split_keys > 0 && kt0 >= kt_end) return;  // (workgroup-uniform) an empty split
+  const int nt = kt_end - kt0;
   const int wcol0 = col0 + wave * 32;
   const int wj_lo = min(wcol0 / g, n - 1);         // earliest token among the wave's columns
   const bool wave_live = wcol0 < ncols;            // the wave has at least one real column
@@ -318,7 +332,7 @@ __device__ __forceinline__ void prefill_item(
                   bf16x8 (&pprev)[2][2], bf16x8 (&pcur)[2][2]) {
     wait_vmem();
     __syncthreads();  // K(kt+1) and V(kt-1) have landed; all waves are done with step kt-1
-    if (kt + 2 < ntiles) issue_k(kt + 2, kt & 1);
+    if (kt + 2 < kt_end) issue_k(kt + 2, kt & 1);
     if constexpr (decltype(has_prev)::value) issue_v(kt, kt & 1);  // V(0): prologue
     if (!wave_live) return;
     const int key0 = kt * kKeys;
@@ -375,10 +389,14 @@ __device__ __forceinline__ void prefill_item(
     lpart += lnew;
   };
 
-  // prologue: K(0), K(1) and V(0) (every buffer is free; their blocks are entries 0..7 of
-  // the first chunk), then Q, all under one wait; scores of tile 0
+  // prologue: K(kt0), K(kt0+1) and V(kt0) (every buffer is free; their blocks are entries
+  // 0..7 of the item's first chunk), then Q, all under one wait; scores of tile kt0
+  if (kt0 > 0) {
+    kchunk_id = vchunk_id = kt0 / 16;
+    kchunk = vchunk = load_chunk(kchunk_id);
+  }
   st.issue(k_cache, sm.k[0], st.kofs, __builtin_amdgcn_readlane(kchunk, slab), hkv, kvh);
-  if (ntiles > 1)
+  if (nt > 1)
     st.issue(k_cache, sm.k[1], st.kofs, __builtin_amdgcn_readlane(kchunk, 4 + slab), hkv, kvh);
   st.issue(v_cache, sm.v[0], st.vofs, __builtin_amdgcn_readlane(kchunk, slab), hkv, kvh);
   // Q fragments; a lane past the last column computes with zeros
@@ -396,16 +414,16 @@ __device__ __forceinline__ void prefill_item(
   using yes = std::true_type;
   using no = std::false_type;
   // step kt consumes scores sa/sb alternately and writes weights pa/pb alternately
-  if (ntiles == 1) {
-    step(no(), no(), 0, sa, sb, pb, pa);
+  if (nt == 1) {
+    step(no(), no(), kt0, sa, sb, pb, pa);
   } else {
-    step(no(), yes(), 0, sa, sb, pb, pa);
-    int kt = 1;
-    for (; kt + 2 < ntiles; kt += 2) {
+    step(no(), yes(), kt0, sa, sb, pb, pa);
+    int kt = kt0 + 1;
+    for (; kt + 2 < kt_end; kt += 2) {
       step(yes(), yes(), kt, sb, sa, pa, pb);
       step(yes(), yes(), kt + 1, sa, sb, pb, pa);
     }
-    if (kt + 1 < ntiles) {
+    if (kt + 1 < kt_end) {
       step(yes(), yes(), kt, sb, sa, pa, pb);
       step(yes(), no(), kt + 1, sa, sb, pb, pa);
       kt += 2;
@@ -417,9 +435,9 @@ __device__ __forceinline__ void prefill_item(
   }
   // epilogue: V of the last tile (loaded by the last step) lands; where that tile reaches
   // past the sequence, zero the V slots >= len (they may hold any bits); then its value
-  // product, with the weights in pa when ntiles is odd and in pb when it is even
+  // product, with the weights in pa when nt is odd and in pb when it is even
   {
-    const int kt = ntiles - 1;
+    const int kt = kt_end - 1;
     wait_vmem();
     __syncthreads();
     if ((kt + 1) * kKeys > len) {
@@ -444,7 +462,7 @@ __device__ __forceinline__ void prefill_item(
       __syncthreads();
     }
     if (wave_live) {
-      if (ntiles & 1) values(kt & 1, pa);
+      if (nt & 1) values(kt & 1, pa);
       else values(kt & 1, pb);
     }
   }
@@ -465,6 +483,32 @@ __device__ __forceinline__ void prefill_item(
   int ln;
   asm volatile("v_and_b32 %0, 63, %1" : "=v"(ln) : "v"((int)threadIdx.x));
   const int lcl = ln & 31, hhl = ln >> 5;
+  if (split_keys > 0) {
+    // rows that reach past split 0 leave this split's partial result (when they reach into
+    // it): the unnormalised output, the running maximum and the weight sum
+    const int gcp = wcol0 + lcl;
+    const int jp = gcp / g;
+    if (gcp < ncols && p + jp >= split_keys && p + jp >= kt0 * kKeys) {
+      const size_t slot =
+          ((size_t)(row0 + jp) * hq + kvh * g + gcp % g) * (size_t)nsplit + (size_t)split;
+      float* wo = ws_o + slot * D + 4 * hhl;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+          st16(wo + 32 * db + 8 * a,
+               u32x4{__float_as_uint(o[db][4 * a + 0]), __float_as_uint(o[db][4 * a + 1]),
+                     __float_as_uint(o[db][4 * a + 2]), __float_as_uint(o[db][4 * a + 3])});
+      if (hhl == 0) {
+        ws_ml[slot * 2 + 0] = m;
+        ws_ml[slot * 2 + 1] = l;
+      }
+    }
+    if (split > 0) return;  // only split 0 holds rows that end in it
+  }
+  // rows that end in this item: every row without a split, and the rows of split 0 whose
+  // keys all fall in it (gc: a column of the item)
+  auto row_ends_here = [&](int gc) { return split_keys == 0 || p + gc / g < split_keys; };
   {
     const float inv = 1.f / l;  // columns past the end: any value, never stored
 #pragma unroll
@@ -484,13 +528,13 @@ __device__ __forceinline__ void prefill_item(
     const int u = ln % CH;
     const u32x4 v = ld16(tile + r * D + ((u ^ (r % CH)) * 8));
     const int gc = wcol0 + r;
-    if (gc < ncols) {
+    if (gc < ncols && row_ends_here(gc)) {
       const int jr = gc / g;
       st16(out + ((size_t)(row0 + jr) * hq + kvh * g + gc % g) * D + u * 8, v);
     }
   }
   const int gcl = wcol0 + lcl;  // this lane's column, recomputed like the lane index
-  if (lse != nullptr && hhl == 0 && gcl < ncols)
+  if (lse != nullptr && hhl == 0 && gcl < ncols && row_ends_here(gcl))
     lse[(size_t)(row0 + gcl / g) * hq + kvh * g + gcl % g] = (m + log2f(l)) * kLn2;
 }
 
@@ -502,7 +546,9 @@ __device__ __forceinline__ void prefill_body(const uint16_t* __restrict__ q, con
                     int32_t max_blocks, const int32_t* __restrict__ cached_lens,
                     const int32_t* __restrict__ cu_new_lens, int32_t num_seqs, int32_t hq,
                     int32_t hkv, int32_t num_blocks, int32_t qtiles, float scale_log2,
-                    uint16_t* __restrict__ out, float* __restrict__ lse, const unsigned wg) {
+                    uint16_t* __restrict__ out, float* __restrict__ lse, const unsigned wg,
+                    int32_t split_keys = 0, int32_t nsplit = 1, float* __restrict__ ws_o = nullptr,
+                    float* __restrict__ ws_ml = nullptr) {
   __shared__ __align__(16) PrefillSmem<D> sm;
   // XCD-aware mapping: workgroup id b runs on XCD b % 8 (a mixed launch passes a `wg` with
   // the same residue mod 8 as its workgroup id). The unit that must stay on one XCD
@@ -515,11 +561,16 @@ __device__ __forceinline__ void prefill_body(const uint16_t* __restrict__ q, con
   // and without the rotation slot s of every group -- and with it the low tiles, the ones
   // every sequence has -- would always land on the same engine, which then fills first and
   // stalls the rotation while the others have free slots.
+  // With a key split a group holds qtiles x nsplit items: each query tile's splits follow
+  // one another in the list.
+  const int per = qtiles * nsplit;         // items per group
   const int xcd = wg & 7;
   const int pos = wg >> 3;                 // position in this XCD's list
-  const int gpos = pos / qtiles;           // the group's place in this XCD's list
+  const int gpos = pos / per;              // the group's place in this XCD's list
   const int group = gpos * 8 + xcd;        // (sequence, kv head) group index
-  const int qt = qtiles - 1 - (pos % qtiles + gpos) % qtiles;
+  const int idx = (pos % per + gpos) % per;
+  const int qt = qtiles - 1 - idx / nsplit;
+  const int sp = idx % nsplit;
   if (group >= num_seqs * hkv) return;
   const int kvh = group % hkv;
   const int i = group / hkv;
@@ -533,20 +584,23 @@ __device__ __forceinline__ void prefill_body(const uint16_t* __restrict__ q, con
   const int n = cu_new_lens[i + 1] - row0;
   if (qt * kCols >= n * (hq / hkv)) return;
   prefill_item<D>(q, k_cache, v_cache, block_tables, max_blocks, hq, hkv, num_blocks, scale_log2,
-                  out, lse, i, kvh, qt, p, row0, n, t_first, t_lane, sm);
+                  out, lse, i, kvh, qt, p, row0, n, t_first, t_lane, sm, split_keys, sp, nsplit,
+                  ws_o, ws_ml);
 }
 
 // The work list of a prefill batch: query tiles per (sequence, kv head) group, and the
-// number of workgroups (the groups dealt to 8 XCD lists of equal length, qtiles each).
+// number of workgroups (the groups dealt to 8 XCD lists of equal length, qtiles x nsplit
+// each).
 struct PrefillGrid {
   int64_t qtiles;
   int64_t items;
 };
-inline PrefillGrid prefill_grid(int32_t hq, int32_t hkv, int32_t num_seqs, int32_t max_new_len) {
+inline PrefillGrid prefill_grid(int32_t hq, int32_t hkv, int32_t num_seqs, int32_t max_new_len,
+                                int32_t nsplit = 1) {
   const int32_t g = hq / hkv;
   const int64_t qtiles = ((int64_t)max_new_len * g + kCols - 1) / kCols;
   const int64_t groups = (int64_t)hkv * num_seqs;
-  return PrefillGrid{qtiles, (groups + 7) / 8 * 8 * qtiles};
+  return PrefillGrid{qtiles, (groups + 7) / 8 * 8 * qtiles * nsplit};
 }
 
 }  // namespace pre

@@ -335,6 +335,31 @@ def test_decode_workspace_is_a_function_of_sizes(lib):
     assert lib.pkv_prefill_workspace_bytes(256, 40000, 32, 8, 128, 256, 1280) == 0
 
 
+def test_prefill_key_split_plan(lib):
+    """The prefill splits keys only when its work items cannot fill the chip (fewer than 1024:
+    sequences x kv heads x 128-column query tiles) and the keys are long; the split size is a
+    multiple of 1024 keys. The five workload shapes never split; small batches of long
+    sequences do, with fp32 partials of (head_dim + 2) per row, head and split."""
+    ws = lib.pkv_prefill_workspace_bytes
+    # Llama-3-8B prefill, mixed 70B-shaped prefill, long documents, tiny: no split
+    assert ws(256, 40935, 32, 8, 128, 256, 1280) == 0
+    assert ws(128, 40934, 64, 8, 128, 512, 2560) == 0
+    assert ws(64, 20561, 32, 8, 128, 512, 16896) == 0
+    assert ws(8, 320, 4, 2, 64, 64, 192) == 0
+    # 2 sequences x 8 kv heads x 5 query tiles = 80 items: 13 wanted, 1024-key splits, 10 of
+    # them over 9250 keys
+    assert ws(2, 187, 32, 8, 128, 150, 9250) == 187 * 32 * 10 * 130 * 4
+    # 752 items: 2 wanted -> 1550 keys, rounded up to 2048: 2 splits
+    assert ws(1, 3000, 32, 8, 128, 3000, 3100) == 3000 * 32 * 2 * 130 * 4
+    # short keys never split; 1016 items (one query tile short of 8 x 128) split in two,
+    # 1024 items do not
+    assert ws(1, 10, 32, 8, 128, 10, 2047) == 0
+    assert ws(1, 4064, 32, 8, 128, 4064, 8192) == 4064 * 32 * 2 * 130 * 4
+    assert ws(1, 4096, 32, 8, 128, 4096, 8192) == 0
+    # head dim 64, one query head per kv head: 3 x 4 x 2 = 24 items, 7 splits over 6200 keys
+    assert ws(3, 265, 4, 4, 64, 200, 6200) == 265 * 4 * 7 * 66 * 4
+
+
 def test_noalloc_decode_refuses_oversize_calls_on_the_host(lib):
     """The allocation-free decode's fixed scratch holds PKV_DECODE_NOALLOC_MAX_BYTES; a call
     needing more is refused before any launch (so no GPU is touched here), with the size in

@@ -177,4 +177,18 @@ LONG_DOC_SHARED_PROMPT = WorkloadSpec(
 )
 
 ALL = (TINY, LLAMA3_8B_PREFILL, LLAMA3_8B_DECODE, MIXED_70B, LONG_DOC_SHARED_PROMPT)
-BY_NAME = {w.name: w for w in ALL}
+
+# Beyond the five: a batch too small to fill the chip, made of very long cached documents
+# with a short downstream suffix each (the case the prefill's key split is for).
+LONG_PREFIX_FEW_TUPLES = WorkloadSpec(
+    name="long_prefix_few_tuples",
+    index=6,
+    num_q_heads=32,
+    num_kv_heads=8,
+    head_dim=128,
+    batches=(BatchSpec("prefill", 4, Dist.uniform(24576, 32768), Dist.uniform(64, 256)),),
+    pool=("scale", 1.25),
+    description="4 tuples, 32/8 heads, head_dim 128, prefix U[24576,32768], new U[64,256]",
+)
+EXTRA = (LONG_PREFIX_FEW_TUPLES,)
+BY_NAME = {w.name: w for w in ALL + EXTRA}
