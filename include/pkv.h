@@ -268,7 +268,7 @@ pkv_status pkv_kv_append(const pkv_paged_kv* kv, const void* k_new, const void* 
  * P_i + N_i.
  * Key split (optional): a batch whose work items -- sequences x kv heads x tiles of 128
  * query columns, a column being one (new token, query head of the kv group) -- number
- * fewer than 1024 cannot keep the chip busy; when its keys are long (max_total_len >= 2048)
+ * fewer than 2048 cannot keep the chip busy; when its keys are long (max_total_len >= 2048)
  * and the caller passes a workspace of at least pkv_prefill_workspace_bytes (16-byte
  * aligned, caller-owned, not read back), every item's keys are cut at multiples of a split
  * size (a multiple of 1024 keys chosen from the host arguments) into parts run as separate

@@ -18,6 +18,12 @@ from tests.test_gpu_prefill import _edge_spec, check, oracle_prefill
 pytestmark = pytest.mark.gpu
 
 
+def nsplit_of(case, nbytes):
+    """The number of splits a workspace size stands for."""
+    b = case.batches[0]
+    return nbytes // (b.total_new * case.hq * (case.d + 2) * 4)
+
+
 def split_bytes(lib, case):
     b = case.batches[0]
     return lib.pkv_prefill_workspace_bytes(b.n_seqs, b.total_new, case.hq, case.hkv, case.d,
@@ -52,7 +58,8 @@ SPLIT_CASES = [
     # one query head per kv head, head dim 64: prefixes ending at (2047), just past (1024 + 1)
     # and well past a boundary; a single new token
     ("mha_d64", 4, 4, 64, [2047, 1025, 6000], [1, 64, 200]),
-    # 8 query heads per kv head, split size 2048: one sequence ends in the first split
+    # 8 query heads per kv head, split size 1024: the first token of one sequence ends in the
+    # first split (its last key is 1023), the next one does not
     ("gqa8_ragged", 64, 8, 128, [1023, 4100], [17, 260]),
 ]
 
@@ -86,14 +93,15 @@ def test_split_is_deterministic_and_agrees_with_unsplit(gpu_lib):
 
 
 # (sequence, query token j, token index of the planted key, visible?) with 8 query / 2 kv
-# heads, three sequences of P = 100 cached and N = 3000 new tokens: the split size is 2048
-# keys, so key positions 2047 | 2048 sit on both sides of the boundary.
+# heads, three sequences of P = 100 cached and N = 3000 new tokens: 564 work items, so the
+# keys are cut into 4 splits of 1024, and key positions 1023 | 1024 (token indices
+# 923 | 924) sit on both sides of the first boundary.
 SPIKES = [
-    (0, 1947, 1947, True),    # a row ending in the first split sees its last key (2047)
-    (0, 1947, 1948, False),   # ... and not the first key of the next split
-    (1, 1948, 1948, True),    # a merged row sees the first key of its second split
-    (1, 1948, 1949, False),
-    (2, 2500, 1947, True),    # a merged row sees a key at the end of its first split
+    (0, 923, 923, True),      # a row ending in the first split sees its last key (1023)
+    (0, 923, 924, False),     # ... and not the first key of the next split
+    (1, 924, 924, True),      # a merged row sees the first key of its second split
+    (1, 924, 925, False),
+    (2, 2500, 923, True),     # a merged row sees a key at the end of its first split
     (2, 2500, 2501, False),
 ]
 
@@ -116,7 +124,7 @@ def test_split_spike_probes_at_boundary(gpu_lib, probe):
     b.k_new[krow, h // 4] = (spike.view(np.uint32) >> 16).astype(np.uint16)
     b.v_new[krow, h // 4] = np.uint16(0x4120)  # 10.0
     out, lse, nbytes = run(gpu_lib, case)
-    assert nbytes > 0
+    assert nsplit_of(case, nbytes) == 4
     o = bf16_to_f64(out)
     ref, _ = oracle_prefill(case)
     if visible:
@@ -128,9 +136,9 @@ def test_split_spike_probes_at_boundary(gpu_lib, probe):
 
 def test_split_long_prefix_few_tuples_full_size(gpu_lib):
     """The workload the split is for, at full size (4 tuples of 24-32k cached tokens, short
-    suffixes: 224 work items, so 5 splits of 7168 keys), against the oracle."""
+    suffixes: 224 work items, so 8 splits of 4096 keys), against the oracle."""
     say("[prefill split] long_prefix_few_tuples, full size")
     case = W.make_case(W.LONG_PREFIX_FEW_TUPLES)
     out, lse, nbytes = run(gpu_lib, case)
-    assert nbytes > 0
+    assert nsplit_of(case, nbytes) == 8
     check("long_prefix_few_tuples", case, (out, lse), oracle_prefill(case))
