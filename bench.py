@@ -778,9 +778,13 @@ def profile_kernel(args, lib, torch):
         out = torch.empty((b.total_new, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
         lib.pkv_kv_append(pk, pv, b.k_new, b.v_new, dv["tables"], dv["cached"], dv["cu"],
                           dv["max_new"])
+        # the workspace that enables the key split, for a batch too small to fill the chip
+        nb = lib.pkv_prefill_workspace_bytes(b.n_seqs, b.total_new, wl.hq, wl.hkv, wl.d,
+                                             dv["max_new"], dv["max_total"])
+        pws = lib.alloc_workspace(nb) if nb else None
         fn = lambda: lib.pkv_prefill_attention(pk, pv, b.q, dv["tables"], dv["cached"],
                                                dv["cu"], dv["max_new"], dv["max_total"],
-                                               wl.scale, out)
+                                               wl.scale, out, workspace=pws)
     else:
         seq_lens = b.prefix_lens + 1
         maxl = int(seq_lens.max())
