@@ -339,6 +339,9 @@ __device__ __forceinline__ void prefill_item(
     if (key0 + kKeys - 1 > p + wj_lo) mask_tile(key0, cur);
 
     // ---- the straight-line block ----
+    // (at a raised wave priority: when both waves on a SIMD can issue, the one in its block of
+    // matrix-core work goes first; 1-1.6% faster on the Llama-3-8B and 70B-shaped layers)
+    __builtin_amdgcn_s_setprio(2);
     if constexpr (decltype(has_next)::value) scores((kt + 1) & 1, nxt);
     if constexpr (decltype(has_prev)::value) values((kt - 1) & 1, pprev);
     float lnew = weights(cur, pcur);
@@ -361,6 +364,7 @@ __device__ __forceinline__ void prefill_item(
         __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // 3 VALU
       }
     }
+    __builtin_amdgcn_s_setprio(0);
     // The running maximum only has to move when some weight of the tile exceeds 2^threshold,
     // and then this lane's (non-negative) weight sum exceeds it too: test the sum, and only
     // then find the tile's exact maximum (the first tile, where m = -inf, always does).
