@@ -512,17 +512,22 @@ def secondary(args, lib, torch, flush):
                       "tuples_per_s": B / med(step)}
     del wl, pk, pv
 
-    # long documents with a shared 512-token prompt
+    # long documents with a shared 512-token prompt (with the workspace that lets the prefill
+    # take its sequences longest first)
     spec = W.LONG_DOC_SHARED_PROMPT
     wl = Workload(spec, lib, torch)
     b, _ = wl.batches[0]
     dv = wl.dev[0]
     pk, pv = wl.case.pool_k, wl.case.pool_v
     o = torch.empty((b.total_new, wl.hq, wl.d), dtype=torch.bfloat16, device="cuda")
+    nb = lib.pkv_prefill_workspace_bytes(b.n_seqs, b.total_new, wl.hq, wl.hkv, wl.d,
+                                         dv["max_new"], dv["max_total"])
+    lws = lib.alloc_workspace(nb) if nb else None
     fns = [lambda: lib.pkv_kv_append(pk, pv, b.k_new, b.v_new, dv["tables"], dv["cached"],
                                      dv["cu"], dv["max_new"]),
            lambda: lib.pkv_prefill_attention(pk, pv, b.q, dv["tables"], dv["cached"], dv["cu"],
-                                             dv["max_new"], dv["max_total"], wl.scale, o)]
+                                             dv["max_new"], dv["max_total"], wl.scale, o,
+                                             workspace=lws)]
     _, step, per = time_steps(torch, stream, fns, steps, warm, flush)
     flops = prefill_flops(b.prefix_lens, b.new_lens, wl.hq, wl.d)
     abytes = append_bytes(b.total_new, wl.hkv, wl.d)
@@ -531,8 +536,9 @@ def secondary(args, lib, torch, flush):
                       "append_frac_hbm": abytes / ta / 1e9 / PEAK_HBM_GBS,
                       "prefill_ms": dist(per[:, 1]), "prefill_TFLOP_s": flops / tp / 1e12,
                       "prefill_frac_mfma": flops / tp / 1e12 / PEAK_BF16_TFLOPS,
-                      "tuples_per_s": b.n_seqs / med(step)}
-    del wl, pk, pv
+                      "tuples_per_s": b.n_seqs / med(step),
+                      "prefill_workspace_bytes": nb}
+    del wl, pk, pv, lws
 
     # a batch too small to fill the chip (4 tuples of 24-32k cached tokens, short suffixes):
     # the prefill without a workspace (no key split) and with one (key split + merge)

@@ -67,15 +67,18 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(
   if (lse != nullptr && lane == 0) lse[item] = (mmax + log2f(den)) * kLn2;
 }
 
-// Longest-first sequence order for the decode grid: waves are dispatched in item order, so
-// taking the longest sequences first keeps the launch from ending on a few long waves.
-// Sequences are bucketed by length on a log scale (32 buckets per factor of two), counted,
-// scanned in descending bucket order and scattered; order within a bucket follows the
-// scatter's atomics and may differ from run to run, which the results do not depend on.
+// Longest-first sequence order for a decode or prefill grid: work is dispatched in item
+// order, so taking the longest sequences first keeps the launch from ending on a few long
+// items. A sequence's length is lens[i], plus cu[i + 1] - cu[i] when cu is given (a prefill's
+// cached and new tokens). Sequences are bucketed by length on a log scale (32 buckets per
+// factor of two), counted, scanned in descending bucket order and scattered; order within a
+// bucket follows the scatter's atomics and may differ from run to run, which the results do
+// not depend on.
 constexpr int kOrderBuckets = 2048;
 constexpr int kOrderThreads = 1024;
 __global__ __launch_bounds__(kOrderThreads) void decode_order_kernel(
-    const int32_t* __restrict__ seq_lens, int32_t num_seqs, int32_t* __restrict__ order) {
+    const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ cu, int32_t num_seqs,
+    int32_t* __restrict__ order) {
   __shared__ int count[kOrderBuckets];
   __shared__ int base[kOrderBuckets];
   __shared__ int part[kOrderThreads];
@@ -83,7 +86,7 @@ __global__ __launch_bounds__(kOrderThreads) void decode_order_kernel(
   for (int b = t; b < kOrderBuckets; b += kOrderThreads) count[b] = 0;
   __syncthreads();
   auto bucket_of = [&](int i) {
-    const int len = seq_lens[i];
+    const int len = seq_lens[i] + (cu != nullptr ? cu[i + 1] - cu[i] : 0);
     if (len < 1) return 0;
     return min(1 + (int)(log2f((float)len) * 32.f), kOrderBuckets - 1);
   };
@@ -107,9 +110,6 @@ __global__ __launch_bounds__(kOrderThreads) void decode_order_kernel(
   for (int i = t; i < num_seqs; i += kOrderThreads) order[atomicAdd(&base[bucket_of(i)], 1)] = i;
 }
 
-size_t order_bytes(int32_t num_seqs) {
-  return ((size_t)num_seqs * sizeof(int32_t) + 255) / 256 * 256;
-}
 
 constexpr int kMaxDevices = 64;
 std::mutex g_scratch_mu;
@@ -181,11 +181,20 @@ DecodePlan decode_plan(const KvView& kv, int32_t hq, int32_t num_seqs, int32_t m
   return p;
 }
 
-hipError_t launch_decode_order(const int32_t* seq_lens, int32_t num_seqs, int32_t* order,
-                               hipStream_t stream) {
-  hipLaunchKernelGGL(decode_order_kernel, dim3(1), dim3(kOrderThreads), 0, stream, seq_lens,
+size_t order_bytes(int32_t num_seqs) {
+  return ((size_t)num_seqs * sizeof(int32_t) + 255) / 256 * 256;
+}
+
+hipError_t launch_seq_order(const int32_t* lens, const int32_t* cu, int32_t num_seqs,
+                            int32_t* order, hipStream_t stream) {
+  hipLaunchKernelGGL(decode_order_kernel, dim3(1), dim3(kOrderThreads), 0, stream, lens, cu,
                      num_seqs, order);
   return hipGetLastError();
+}
+
+hipError_t launch_decode_order(const int32_t* seq_lens, int32_t num_seqs, int32_t* order,
+                               hipStream_t stream) {
+  return launch_seq_order(seq_lens, nullptr, num_seqs, order, stream);
 }
 
 hipError_t launch_decode_merge(const KvView& kv, const DecodePlan& p, int32_t hq,

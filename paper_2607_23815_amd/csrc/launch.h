@@ -29,18 +29,21 @@ hipError_t launch_gather_kv(const KvView& kv, const int32_t* block_tables, int32
 hipError_t launch_copy_blocks(const KvView& kv, const int32_t* pairs, int32_t num_pairs,
                               hipStream_t stream);
 
-// Prefill key split: a batch whose work items cannot fill the chip (few sequences, few new
-// tokens) and whose keys are long has each item's keys cut at multiples of split_keys (a
-// multiple of 1024) into nsplit parts, run as separate work items and merged; otherwise
-// split_keys = 0 and nsplit = 1. The plan depends on the host arguments only.
+// Prefill plan, from the host arguments only. Key split: a batch whose work items cannot
+// fill the chip (few sequences, few new tokens) and whose keys are long has each item's keys
+// cut at multiples of split_keys (a multiple of 1024) into nsplit parts, run as separate work
+// items and merged; otherwise split_keys = 0 and nsplit = 1. Order: a batch with long keys
+// (up to at least 8192) takes its sequences longest first.
 struct PrefillSplit {
   int32_t split_keys;
   int32_t nsplit;
+  bool order;
 };
 PrefillSplit prefill_split_plan(int32_t num_seqs, int32_t hq, int32_t hkv, int32_t max_new_len,
                                 int32_t max_total_len);
-// Workspace of a split launch (0 without a split): fp32 partial outputs
-// [total_new][hq][nsplit][head_dim], then their (maximum, weight sum) pairs.
+// Workspace of the plan (0 when it needs none): the sequence order when ordered, then when
+// split the fp32 partial outputs [total_new][hq][nsplit][head_dim] and their (maximum, weight
+// sum) pairs.
 size_t prefill_workspace_bytes(int32_t num_seqs, int32_t total_new, int32_t hq, int32_t hkv,
                                int32_t head_dim, int32_t max_new_len, int32_t max_total_len);
 // With workspace == nullptr the launch does not split.
@@ -69,6 +72,11 @@ DecodePlan decode_plan(const KvView& kv, int32_t hq, int32_t num_seqs, int32_t m
                        void* workspace);
 hipError_t launch_decode_order(const int32_t* seq_lens, int32_t num_seqs, int32_t* order,
                                hipStream_t stream);
+// Longest-first order of sequences by lens[i] (+ cu[i + 1] - cu[i] when cu is given), and the
+// bytes it takes in a workspace (256-byte rounded).
+hipError_t launch_seq_order(const int32_t* lens, const int32_t* cu, int32_t num_seqs,
+                            int32_t* order, hipStream_t stream);
+size_t order_bytes(int32_t num_seqs);
 hipError_t launch_decode_merge(const KvView& kv, const DecodePlan& p, int32_t hq,
                                const int32_t* seq_lens, int32_t num_seqs, uint16_t* out,
                                float* lse, hipStream_t stream);

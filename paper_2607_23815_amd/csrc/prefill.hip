@@ -10,9 +10,9 @@
 namespace pkv {
 namespace {
 
-// kSplit: the launch cuts keys into splits (a separate instantiation, so that the common
-// launch without a split compiles exactly as before)
-template <int D, bool kSplit>
+// kPlan: the launch follows a plan (key splits and/or a longest-first sequence order; a
+// separate instantiation, so that the common launch without either compiles as before)
+template <int D, bool kPlan>
 __global__ __attribute__((amdgpu_flat_work_group_size(pre::kThreads, pre::kThreads),
                           amdgpu_waves_per_eu(2, 2)))
 void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
@@ -21,11 +21,12 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__
                     const int32_t* __restrict__ cu_new_lens, int32_t num_seqs, int32_t hq,
                     int32_t hkv, int32_t num_blocks, int32_t qtiles, float scale_log2,
                     uint16_t* __restrict__ out, float* __restrict__ lse, int32_t split_keys,
-                    int32_t nsplit, float* __restrict__ ws_o, float* __restrict__ ws_ml) {
-  if constexpr (kSplit)
+                    int32_t nsplit, float* __restrict__ ws_o, float* __restrict__ ws_ml,
+                    const int32_t* __restrict__ order) {
+  if constexpr (kPlan)
     pre::prefill_body<D>(q, k_cache, v_cache, block_tables, max_blocks, cached_lens,
                          cu_new_lens, num_seqs, hq, hkv, num_blocks, qtiles, scale_log2, out,
-                         lse, blockIdx.x, split_keys, nsplit, ws_o, ws_ml);
+                         lse, blockIdx.x, split_keys, nsplit, ws_o, ws_ml, order);
   else
     pre::prefill_body<D>(q, k_cache, v_cache, block_tables, max_blocks, cached_lens,
                          cu_new_lens, num_seqs, hq, hkv, num_blocks, qtiles, scale_log2, out,
@@ -95,13 +96,18 @@ __global__ __launch_bounds__(256) void prefill_merge_kernel(
 constexpr int64_t kFillItems = 2048;
 constexpr int32_t kSplitUnit = 1024;   // split_keys is a multiple of this (one table chunk)
 constexpr int32_t kMaxSplits = 64;
+// Keys from which a batch's sequences are taken longest first (a one-workgroup ordering
+// kernel and one more dependent load per workgroup): with documents up to 16k keys the
+// longest items would otherwise start anywhere in the launch and extend its end.
+constexpr int32_t kOrderKeys = 8192;
 
 PrefillSplit prefill_split_plan(int32_t num_seqs, int32_t hq, int32_t hkv, int32_t max_new_len,
                                 int32_t max_total_len) {
-  const PrefillSplit none{0, 1};
-  if (num_seqs <= 0 || hkv <= 0 || hq % hkv != 0 || max_new_len <= 0 ||
-      max_total_len < 2 * kSplitUnit)
-    return none;
+  if (num_seqs <= 0 || hkv <= 0 || hq % hkv != 0 || max_new_len <= 0)
+    return PrefillSplit{0, 1, false};
+  const bool order = max_total_len >= kOrderKeys && num_seqs > 1;
+  const PrefillSplit none{0, 1, order};
+  if (max_total_len < 2 * kSplitUnit) return none;
   const pre::PrefillGrid pg = pre::prefill_grid(hq, hkv, num_seqs, max_new_len);
   const int64_t items = (int64_t)num_seqs * hkv * pg.qtiles;
   if (items >= kFillItems) return none;
@@ -110,14 +116,16 @@ PrefillSplit prefill_split_plan(int32_t num_seqs, int32_t hq, int32_t hkv, int32
   keys = (keys + kSplitUnit - 1) / kSplitUnit * kSplitUnit;
   const int64_t nsplit = (max_total_len + keys - 1) / keys;
   if (nsplit <= 1) return none;
-  return PrefillSplit{(int32_t)keys, (int32_t)nsplit};
+  return PrefillSplit{(int32_t)keys, (int32_t)nsplit, order};
 }
 
 size_t prefill_workspace_bytes(int32_t num_seqs, int32_t total_new, int32_t hq, int32_t hkv,
                                int32_t head_dim, int32_t max_new_len, int32_t max_total_len) {
   const PrefillSplit sp = prefill_split_plan(num_seqs, hq, hkv, max_new_len, max_total_len);
-  if (sp.nsplit <= 1 || total_new <= 0) return 0;
-  return (size_t)total_new * hq * sp.nsplit * (head_dim + 2) * sizeof(float);
+  if (total_new <= 0) return 0;
+  size_t bytes = sp.order ? order_bytes(num_seqs) : 0;
+  if (sp.nsplit > 1) bytes += (size_t)total_new * hq * sp.nsplit * (head_dim + 2) * sizeof(float);
+  return bytes;
 }
 
 hipError_t launch_prefill(const KvView& kv, const uint16_t* q, int32_t hq,
@@ -126,27 +134,35 @@ hipError_t launch_prefill(const KvView& kv, const uint16_t* q, int32_t hq,
                           int32_t num_seqs, int32_t total_new, int32_t max_new_len,
                           int32_t max_total_len, float scale, uint16_t* out, float* lse,
                           void* workspace, hipStream_t stream) {
-  PrefillSplit sp{0, 1};
+  PrefillSplit sp{0, 1, false};
   if (workspace != nullptr)
     sp = prefill_split_plan(num_seqs, hq, kv.hkv, max_new_len, max_total_len);
+  int32_t* order = nullptr;
   float* ws_o = nullptr;
   float* ws_ml = nullptr;
+  char* ws = static_cast<char*>(workspace);
+  if (sp.order) {
+    order = reinterpret_cast<int32_t*>(ws);
+    ws += order_bytes(num_seqs);
+    const hipError_t err = launch_seq_order(cached_lens, cu_new_lens, num_seqs, order, stream);
+    if (err != hipSuccess) return err;
+  }
   if (sp.nsplit > 1) {
-    ws_o = static_cast<float*>(workspace);
+    ws_o = reinterpret_cast<float*>(ws);
     ws_ml = ws_o + (size_t)total_new * hq * sp.nsplit * kv.head_dim;
   }
+  const bool plan = sp.order || sp.nsplit > 1;
   const pre::PrefillGrid pg = pre::prefill_grid(hq, kv.hkv, num_seqs, max_new_len, sp.nsplit);
   if (pg.items > INT32_MAX) return hipErrorInvalidValue;
   const int64_t qtiles = pg.qtiles;
   const dim3 grid((unsigned)pg.items);
   const float scale_log2 = scale * kLog2e;
-  auto* kern = kv.head_dim == 128
-                   ? (sp.nsplit > 1 ? prefill_kernel<128, true> : prefill_kernel<128, false>)
-                   : (sp.nsplit > 1 ? prefill_kernel<64, true> : prefill_kernel<64, false>);
+  auto* kern = kv.head_dim == 128 ? (plan ? prefill_kernel<128, true> : prefill_kernel<128, false>)
+                                  : (plan ? prefill_kernel<64, true> : prefill_kernel<64, false>);
   hipLaunchKernelGGL(kern, grid, dim3(pre::kThreads), 0, stream, q, kv.k, kv.v, block_tables,
                      max_blocks, cached_lens, cu_new_lens, num_seqs, hq, kv.hkv, kv.num_blocks,
                      (int32_t)qtiles, scale_log2, out, lse, sp.split_keys, sp.nsplit, ws_o,
-                     ws_ml);
+                     ws_ml, order);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess || sp.nsplit <= 1) return err;
   const dim3 mgrid((unsigned)(((int64_t)max_new_len * hq + 3) / 4), (unsigned)num_seqs);

@@ -553,7 +553,8 @@ __device__ __forceinline__ void prefill_body(const uint16_t* __restrict__ q, con
                     int32_t hkv, int32_t num_blocks, int32_t qtiles, float scale_log2,
                     uint16_t* __restrict__ out, float* __restrict__ lse, const unsigned wg,
                     int32_t split_keys = 0, int32_t nsplit = 1, float* __restrict__ ws_o = nullptr,
-                    float* __restrict__ ws_ml = nullptr) {
+                    float* __restrict__ ws_ml = nullptr,
+                    const int32_t* __restrict__ order = nullptr) {
   __shared__ __align__(16) PrefillSmem<D> sm;
   // XCD-aware mapping: workgroup id b runs on XCD b % 8 (a mixed launch passes a `wg` with
   // the same residue mod 8 as its workgroup id). The unit that must stay on one XCD
@@ -578,7 +579,8 @@ __device__ __forceinline__ void prefill_body(const uint16_t* __restrict__ q, con
   const int sp = idx % nsplit;
   if (group >= num_seqs * hkv) return;
   const int kvh = group % hkv;
-  const int i = group / hkv;
+  // with an order, group ranks map to sequences longest first
+  const int i = order != nullptr ? order[group / hkv] : group / hkv;
   // The first table chunk (entry `lane` of the sequence's row, and entry 0) is fetched
   // before the lengths: its address depends on the sequence only, so the two loads overlap.
   const int32_t* table = block_tables + (size_t)i * max_blocks;

@@ -335,26 +335,30 @@ def test_decode_workspace_is_a_function_of_sizes(lib):
     assert lib.pkv_prefill_workspace_bytes(256, 40000, 32, 8, 128, 256, 1280) == 0
 
 
-def test_prefill_key_split_plan(lib):
+def test_prefill_plan(lib):
     """The prefill splits keys only when its work items cannot fill the chip (fewer than 2048:
     sequences x kv heads x 128-column query tiles) and the keys are long; the split size is a
-    multiple of 1024 keys. The five workload shapes never split; small batches of long
-    sequences do, with fp32 partials of (head_dim + 2) per row, head and split."""
+    multiple of 1024 keys. Batches of several sequences whose keys reach 8192 are ordered
+    longest first. The workspace holds the order (int32 per sequence, 256-byte rounded), then
+    fp32 partials of (head_dim + 2) per row, head and split. Of the five workload shapes only
+    the long documents are ordered, and none splits."""
     ws = lib.pkv_prefill_workspace_bytes
-    # Llama-3-8B prefill, mixed 70B-shaped prefill, long documents, tiny: no split
+    # Llama-3-8B prefill, mixed 70B-shaped prefill, tiny: nothing; long documents: the order
     assert ws(256, 40935, 32, 8, 128, 256, 1280) == 0
     assert ws(128, 40934, 64, 8, 128, 512, 2560) == 0
-    assert ws(64, 20561, 32, 8, 128, 512, 16896) == 0
     assert ws(8, 320, 4, 2, 64, 64, 192) == 0
+    assert ws(64, 20561, 32, 8, 128, 512, 16896) == 256
     # 2 sequences x 8 kv heads x 5 query tiles = 80 items: 26 wanted, 1024-key splits, 10 of
-    # them over 9250 keys
-    assert ws(2, 187, 32, 8, 128, 150, 9250) == 187 * 32 * 10 * 130 * 4
+    # them over 9250 keys; ordered
+    assert ws(2, 187, 32, 8, 128, 150, 9250) == 256 + 187 * 32 * 10 * 130 * 4
     # 752 items: 3 wanted -> 1034 keys, rounded up to 2048: 2 splits
     assert ws(1, 3000, 32, 8, 128, 3000, 3100) == 3000 * 32 * 2 * 130 * 4
-    # short keys never split; 1016 items split in three (2731 keys -> 3072), 2048 do not
+    # short keys never split; 1016 items split in three (2731 keys -> 3072; one sequence: no
+    # order); 2048 items do not split (two sequences of 8192 keys: ordered)
     assert ws(1, 10, 32, 8, 128, 10, 2047) == 0
     assert ws(1, 4064, 32, 8, 128, 4064, 8192) == 4064 * 32 * 3 * 130 * 4
-    assert ws(2, 8192, 32, 8, 128, 4096, 8192) == 0
+    assert ws(2, 8192, 32, 8, 128, 4096, 8192) == 256
+    assert ws(2, 8192, 32, 8, 128, 4096, 8191) == 0
     # head dim 64, one query head per kv head: 3 x 4 x 2 = 24 items, 7 splits over 6200 keys
     assert ws(3, 265, 4, 4, 64, 200, 6200) == 265 * 4 * 7 * 66 * 4
 

@@ -1,4 +1,5 @@
-"""GPU tier: the prefill key split, through the C ABI, against the fp64 oracle.
+"""GPU tier: the prefill's plan (key split, longest-first order), through the C ABI, against
+the fp64 oracle.
 
 A batch whose work items cannot fill the chip (few sequences, few new tokens) and whose keys
 are long runs with its keys cut at multiples of a split size when the caller passes the
@@ -142,3 +143,20 @@ def test_split_long_prefix_few_tuples_full_size(gpu_lib):
     out, lse, nbytes = run(gpu_lib, case)
     assert nsplit_of(case, nbytes) == 8
     check("long_prefix_few_tuples", case, (out, lse), oracle_prefill(case))
+
+
+def test_ordered_prefill_is_bit_identical(gpu_lib):
+    """With a workspace, a batch whose keys reach 8192 takes its sequences longest first (2048
+    work items here, so no split): the order moves work items, not arithmetic, so the output is
+    bit-identical to the launch without a workspace, and meets the bar against the oracle."""
+    say("[prefill plan] longest-first order")
+    prefixes = [300, 9000, 40, 5000, 1200, 7000, 16, 2500, 600, 8100, 64, 3000, 90, 4000, 128, 6000]
+    news = [512, 17, 300, 128, 64, 512, 1, 200, 480, 33, 256, 100, 512, 7, 150, 90]
+    spec = _edge_spec("order", 190, 32, 8, 128, len(prefixes))
+    case = W.make_case(spec, prefix_override=[prefixes], new_override=[news])
+    a = run(gpu_lib, case)
+    assert a[2] == 256, "ordered, not split"
+    u = run(gpu_lib, W.make_case(spec, prefix_override=[prefixes], new_override=[news]),
+            split=False)
+    assert np.array_equal(a[0], u[0]) and np.array_equal(a[1], u[1])
+    check("ordered", case, a[:2], oracle_prefill(case))
