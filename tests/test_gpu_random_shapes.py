@@ -4,7 +4,8 @@ Each case draws a kv-head count, a query/kv head ratio (1 to 16), a head dim (64
 batch size, per-sequence prefix and suffix lengths (prefixes ending anywhere in a block,
 empty prefixes included) and a random block placement. The append is checked bit for bit
 over the whole pool (every byte outside the new slots unchanged, NaN canaries included),
-prefill and decode against the fp64 oracle at the same bar as the other GPU tests."""
+prefill and decode against the fp64 oracle at the same bar as the other GPU tests; a sweep of
+small batches of long sequences runs the prefill with its plan (key split, order)."""
 import numpy as np
 import pytest
 
@@ -79,3 +80,45 @@ def test_random_decode(gpu_lib, k):
     say(f"[random] decode {k}: hq={case.hq} hkv={case.hkv} d={case.d} seqs={b.n_seqs} "
         f"max context={int(b.prefix_lens.max())}")
     check_decode(f"random_decode_{k}", run_decode(gpu_lib, case), oracle_decode(case))
+
+
+def _plan_case(k):
+    """A small batch of long sequences: the prefill's plan splits its keys (and, when several
+    sequences reach 8192 keys, orders them longest first)."""
+    rng = np.random.default_rng(SEED + 200 + k)
+    hq, hkv, d = _heads(rng)
+    b = int(rng.integers(1, 4))
+    prefixes = rng.integers(2100, 12000, b)
+    news = rng.integers(1, 160, b)
+    spec = W.WorkloadSpec(f"random_plan_{k}", 1100 + k, hq, hkv, d,
+                          (W.BatchSpec("prefill", b, W.Dist.const(1), W.Dist.const(1)),),
+                          ("scale", 1.25))
+    return W.make_case(spec, prefix_override=[prefixes.tolist()],
+                       new_override=[news.tolist()])
+
+
+@pytest.mark.parametrize("k", range(8))
+def test_random_prefill_with_plan(gpu_lib, k):
+    """Random small batches of long sequences through the prefill with the plan's workspace
+    (key split, longest-first order) against the oracle."""
+    import torch
+    from tests.gpu_util import scale_for
+    case = _plan_case(k)
+    b = case.batches[0]
+    db = DevBatch(b)
+    nbytes = gpu_lib.pkv_prefill_workspace_bytes(b.n_seqs, b.total_new, case.hq, case.hkv,
+                                                 case.d, db.max_new, db.max_total)
+    say(f"[random] plan {k}: hq={case.hq} hkv={case.hkv} d={case.d} "
+        f"prefix={b.prefix_lens.tolist()} new={b.new_lens.tolist()} workspace={nbytes}")
+    assert nbytes > 0, "the case was meant to split"
+    pk, pv = dev_pools(case)
+    ws = gpu_lib.alloc_workspace(nbytes)
+    out = torch.empty((b.total_new, case.hq, case.d), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((b.total_new, case.hq), dtype=torch.float32, device="cuda")
+    gpu_lib.pkv_kv_append(pk, pv, db.k_new, db.v_new, db.tables, db.cached, db.cu, db.max_new)
+    gpu_lib.pkv_prefill_attention(pk, pv, db.q, db.tables, db.cached, db.cu, db.max_new,
+                                  db.max_total, scale_for(case.d), out, lse=lse, workspace=ws)
+    torch.cuda.synchronize()
+    check_prefill(f"random_plan_{k}", case,
+                  (to_host_bits(out), lse.cpu().numpy().astype(np.float64)),
+                  oracle_prefill(case))
