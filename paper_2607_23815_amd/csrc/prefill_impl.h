@@ -80,6 +80,12 @@ struct PrefillSmem {
   uint16_t v[2][4 * SLAB];
 };
 
+// The steady-state block (below): fragments read this many matrix-core ops ahead, fences
+// every kSub ops, three vector ops scheduled after each matrix-core op. Measured against
+// 5 or 6 reads ahead, fences every 2 or 8 ops, 4 vector ops and no fences: equal within 0.5%
+// or slower (2 ops per fence 1-2%, 4 vector ops 2-4%).
+constexpr int kAhead = 4, kSub = 4, kValu = 3;
+
 // Rescale the running output only when a column's maximum grows by more than this many
 // powers of two; otherwise keep the stale maximum (weights then stay below 2^8, exact in the
 // normalisation). After the first tiles the maximum of N(0,1) scores hardly moves, so the
@@ -317,6 +323,71 @@ __device__ __forceinline__ void prefill_item(
         }
   };
 
+  // The straight-line block of a steady-state step as fenced sub-blocks of kSub matrix-core
+  // ops each: ops 0 .. NQK-1 are the score products of tile kt+1 (K fragment t = (kk, beta) =
+  // (t / 2, t % 2)), ops NQK .. NOPS-1 the value products of tile kt-1 (V fragment t - NQK =
+  // (beta, u, db) in that nesting); 32 ops at head dim 128, 16 at 64. Fragments sit in an
+  // 8-entry register ring and are read kAhead ops ahead, so every op finds its operand landed;
+  // the fences keep the compiler from reordering ops against their reads. The sixteen softmax
+  // slices of tile kt are spread evenly over the sub-blocks (three vector ops per matrix-core
+  // op).
+  constexpr int NQK = 2 * KK, NOPS = NQK + 4 * DB;
+  constexpr int NSUB = NOPS / kSub, SLICES = 16 / NSUB;  // sub-blocks; softmax slices in each
+  static_assert(NOPS % kSub == 0 && 16 % NSUB == 0 && kAhead < 8, "block shape");
+  auto frag = [&](int t, int kbuf, int vbuf) -> u32x4 {
+    if (t < NQK) {
+      const int kk = t >> 1, beta = t & 1;
+      return ld16(&sm.k[kbuf][kread + beta * 2 * SLAB + kk * 256]);
+    }
+    const int f = t - NQK;
+    const int beta = f / (2 * DB), u = (f / DB) & 1, db = f % DB;
+    return ld16(&sm.v[vbuf][(2 * beta + u) * SLAB + vread + db * 512]);
+  };
+  auto fused_block = [&](int kbuf, int vbuf, u32x4 (&fr)[8], f32x16 (&sc)[2],
+                         const bf16x8 (&pprev)[2][2], f32x16 (&cur)[2], bf16x8 (&pcur)[2][2],
+                         float (&sum)[8]) {
+    const float neg_m = -m;
+    u32x4 w[2][2];
+#pragma unroll
+    for (int s = 0; s < NSUB; ++s) {
+#pragma unroll
+      for (int k = 0; k < kSub; ++k) {
+        const int t = kSub * s + k;
+        if (t + kAhead < NOPS) fr[(t + kAhead) & 7] = frag(t + kAhead, kbuf, vbuf);
+        if (t < NQK) {
+          const int kk = t >> 1, beta = t & 1;
+          sc[beta] = mfma32(as_bf16x8(fr[t & 7]), qf[kk], sc[beta]);
+        } else {
+          const int f = t - NQK;
+          const int beta = f / (2 * DB), u = (f / DB) & 1, db = f % DB;
+          o[db] = mfma32(as_bf16x8(fr[t & 7]), pprev[beta][u], o[db]);
+        }
+      }
+#pragma unroll
+      for (int h = 0; h < SLICES; ++h) {
+        const int it = SLICES * s + h;  // softmax slice (beta, u, e)
+        const int beta = it >> 3, u = (it >> 2) & 1, e = it & 3;
+        const float a = fast_exp2(__builtin_fmaf(cur[beta][8 * u + 2 * e], scale_log2, neg_m));
+        const float b = fast_exp2(__builtin_fmaf(cur[beta][8 * u + 2 * e + 1], scale_log2, neg_m));
+        w[beta][u][e] = pack_bf16x2(a, b);
+        asm volatile("" ::"v"(w[beta][u][e]));  // the pack stays in this sub-block
+        sum[2 * e] += a;
+        sum[2 * e + 1] += b;
+      }
+#pragma unroll
+      for (int k = 0; k < kSub; ++k) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+        __builtin_amdgcn_sched_group_barrier(0x002, kValu, 0);  // vector ops
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int beta = 0; beta < 2; ++beta)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) pcur[beta][u] = as_bf16x8(w[beta][u]);
+  };
+
   // One step of the software pipeline, for tile kt. On entry cur holds the raw scores of
   // tile kt and pprev the weights of tile kt-1 (when has_prev). One straight-line block
   // then issues the score MFMAs of tile kt+1 (when has_next) and the value MFMAs of tile
@@ -332,19 +403,39 @@ __device__ __forceinline__ void prefill_item(
                   bf16x8 (&pprev)[2][2], bf16x8 (&pcur)[2][2]) {
     wait_vmem();
     __syncthreads();  // K(kt+1) and V(kt-1) have landed; all waves are done with step kt-1
+    constexpr bool kFused = decltype(has_next)::value && decltype(has_prev)::value;
+    u32x4 fr[8];
+    if constexpr (kFused) {
+      // the first sub-block's K fragments, ahead of the staging issue
+      if (wave_live) {
+#pragma unroll
+        for (int t = 0; t < kAhead; ++t) fr[t] = frag(t, (kt + 1) & 1, (kt - 1) & 1);
+      }
+    }
     if (kt + 2 < kt_end) issue_k(kt + 2, kt & 1);
     if constexpr (decltype(has_prev)::value) issue_v(kt, kt & 1);  // V(0): prologue
     if (!wave_live) return;
     const int key0 = kt * kKeys;
     if (key0 + kKeys - 1 > p + wj_lo) mask_tile(key0, cur);
 
-    // ---- the straight-line block ----
+    // ---- the straight-line block (the fenced sub-blocks above in the steady state) ----
     // (at a raised wave priority: when both waves on a SIMD can issue, the one in its block of
     // matrix-core work goes first; 1-1.6% faster on the Llama-3-8B and 70B-shaped layers)
     __builtin_amdgcn_s_setprio(2);
-    if constexpr (decltype(has_next)::value) scores((kt + 1) & 1, nxt);
-    if constexpr (decltype(has_prev)::value) values((kt - 1) & 1, pprev);
-    float lnew = weights(cur, pcur);
+    float lnew;
+    if constexpr (kFused) {
+      float sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int beta = 0; beta < 2; ++beta)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) nxt[beta][r] = 0.f;
+      fused_block((kt + 1) & 1, (kt - 1) & 1, fr, nxt, pprev, cur, pcur, sum);
+      lnew = ((sum[0] + sum[1]) + (sum[2] + sum[3])) + ((sum[4] + sum[5]) + (sum[6] + sum[7]));
+    } else {
+      if constexpr (decltype(has_next)::value) scores((kt + 1) & 1, nxt);
+      if constexpr (decltype(has_prev)::value) values((kt - 1) & 1, pprev);
+      lnew = weights(cur, pcur);
+    }
     // keep the speculative weights in this block: without a use here the compiler would sink
     // their computation past the rare branch below (which overwrites them), out of reach of
     // the interleave
@@ -352,18 +443,6 @@ __device__ __forceinline__ void prefill_item(
                  "v"(__builtin_bit_cast(u32x4, pcur[0][1])),
                  "v"(__builtin_bit_cast(u32x4, pcur[1][0])),
                  "v"(__builtin_bit_cast(u32x4, pcur[1][1])), "v"(lnew));
-    if constexpr (decltype(has_next)::value && decltype(has_prev)::value) {
-      // interleave: fragment reads ahead, then each of the 32 MFMAs followed by the next
-      // fragment read and a slice of the softmax arithmetic (three vector ops per MFMA,
-      // the rest after the block: measured 2% faster than four, and faster than two or five)
-      __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);    // 6 LDS reads
-#pragma unroll
-      for (int k = 0; k < 32; ++k) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
-        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // 3 VALU
-      }
-    }
     __builtin_amdgcn_s_setprio(0);
     // The running maximum only has to move when some weight of the tile exceeds 2^threshold,
     // and then this lane's (non-negative) weight sum exceeds it too: test the sum, and only
