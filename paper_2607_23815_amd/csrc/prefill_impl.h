@@ -80,8 +80,8 @@ struct PrefillSmem {
   uint16_t v[2][4 * SLAB];
 };
 
-// The steady-state block (below): fragments read this many matrix-core ops ahead, fences
-// every kSub ops, three vector ops scheduled after each matrix-core op. Measured against
+// The matrix-core block of a step (below): fragments read this many matrix-core ops ahead,
+// fences every kSub ops, three vector ops scheduled after each matrix-core op. Measured against
 // 5 or 6 reads ahead, fences every 2 or 8 ops, 4 vector ops and no fences: equal within 0.5%
 // or slower (2 ops per fence 1-2%, 4 vector ops 2-4%).
 constexpr int kAhead = 4, kSub = 4, kValu = 3;
@@ -249,25 +249,6 @@ __device__ __forceinline__ void prefill_item(
   const int kread = (lc >> 4) * SLAB + (hh * 16 + (lc & 15)) * 8;
   const int vread = (2 * lc + (hh ^ ((lc >> 3) & 1))) * 8;
 
-  // scores S^T of the K tile in buffer kbuf, both 32-key halves (two independent chains)
-  auto scores = [&](int kbuf, f32x16 (&sc)[2]) {
-    u32x4 ka[2][KK];
-#pragma unroll
-    for (int beta = 0; beta < 2; ++beta)
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk)
-        ka[beta][kk] = ld16(&sm.k[kbuf][kread + beta * 2 * SLAB + kk * 256]);
-#pragma unroll
-    for (int beta = 0; beta < 2; ++beta)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sc[beta][r] = 0.f;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk)
-#pragma unroll
-      for (int beta = 0; beta < 2; ++beta)
-        sc[beta] = mfma32(as_bf16x8(ka[beta][kk]), qf[kk], sc[beta]);
-  };
-
   // register r of half-tile beta holds the score of key
   // key0 + 32 beta + 16 (r/8) + 8 hh + 4 ((r/4) % 2) + r % 4
   // (compared as a compile-time offset against lim - key0 - 8 hh, so no per-register key
@@ -283,11 +264,8 @@ __device__ __forceinline__ void prefill_item(
       }
   };
 
-  // weights of one tile: P = 2^(scale_log2 * S - m) rounded to bf16 (the value-product
-  // operand), and the sum of the fp32 weights before rounding (each rounded weight is within
-  // a relative 2^-9 of its fp32 value, unbiased). The sum is kept in eight independent
-  // partial sums: a single accumulator would chain dependent adds through the block and
-  // stall the in-order issue that has to keep the matrix cores fed.
+  // weights of one tile outside the block (after a rescale, and on an item's first tile):
+  // the same arithmetic as the block's softmax slices, in the same order
   auto weights = [&](f32x16 (&sc)[2], bf16x8 (&pw)[2][2]) {
     const float neg_m = -m;
     float sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -308,44 +286,49 @@ __device__ __forceinline__ void prefill_item(
       }
     return ((sum[0] + sum[1]) + (sum[2] + sum[3])) + ((sum[4] + sum[5]) + (sum[6] + sum[7]));
   };
-  // value product of one tile: O^T += V^T P^T; step (beta, u) covers block 2 beta + u of the
-  // tile, lane group hh supplying slots 8 hh .. 8 hh + 7 of V^T row 32 db + lc
-  auto values = [&](int vbuf, const bf16x8 (&pw)[2][2]) {
-    const uint16_t* vt = sm.v[vbuf];
-#pragma unroll
-    for (int beta = 0; beta < 2; ++beta)
-#pragma unroll
-      for (int u = 0; u < 2; ++u)
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const u32x4 a = ld16(&vt[(2 * beta + u) * SLAB + vread + db * 512]);
-          o[db] = mfma32(as_bf16x8(a), pw[beta][u], o[db]);
-        }
-  };
-
-  // The straight-line block of a steady-state step as fenced sub-blocks of kSub matrix-core
-  // ops each: ops 0 .. NQK-1 are the score products of tile kt+1 (K fragment t = (kk, beta) =
-  // (t / 2, t % 2)), ops NQK .. NOPS-1 the value products of tile kt-1 (V fragment t - NQK =
-  // (beta, u, db) in that nesting); 32 ops at head dim 128, 16 at 64. Fragments sit in an
-  // 8-entry register ring and are read kAhead ops ahead, so every op finds its operand landed;
-  // the fences keep the compiler from reordering ops against their reads. The sixteen softmax
-  // slices of tile kt are spread evenly over the sub-blocks (three vector ops per matrix-core
-  // op).
-  constexpr int NQK = 2 * KK, NOPS = NQK + 4 * DB;
-  constexpr int NSUB = NOPS / kSub, SLICES = 16 / NSUB;  // sub-blocks; softmax slices in each
-  static_assert(NOPS % kSub == 0 && 16 % NSUB == 0 && kAhead < 8, "block shape");
-  auto frag = [&](int t, int kbuf, int vbuf) -> u32x4 {
-    if (t < NQK) {
+  // The matrix-core work of a step as fenced sub-blocks of kSub ops each: the score products
+  // S^T = K Q^T of the K tile in buffer kbuf (when QK; op t < NQ reads K fragment (kk, beta) =
+  // (t / 2, t % 2), both 32-key halves as two independent chains), then the value products
+  // O^T += V^T P^T of the V tile in buffer vbuf with the weights pw (when PV; op NQ + f reads
+  // V fragment f = (beta, u, db) in that nesting: step (beta, u) covers block 2 beta + u of
+  // the tile, lane group hh supplying slots 8 hh .. 8 hh + 7 of V^T row 32 db + lc). 32 ops
+  // in a steady-state step at head dim 128, 16 at 64. Fragments sit in an 8-entry register
+  // ring and are read kAhead ops ahead (the first kAhead by the caller unless PRE), so every
+  // op finds its operand landed; the fences keep the compiler from reordering ops against
+  // their reads. With SM the sixteen slices of the softmax of the scores in cur are spread
+  // evenly over the sub-blocks (kValu vector ops after each matrix-core op): weights
+  // P = 2^(scale_log2 * S - m) rounded to bf16 into pcur, and the sums of the fp32 weights
+  // before rounding in eight independent partial sums (each rounded weight is within a
+  // relative 2^-9 of its fp32 value, unbiased; a single accumulator would chain dependent
+  // adds through the block).
+  using yes_t = std::true_type;
+  using no_t = std::false_type;
+  auto frag = [&](auto nq, int t, int kbuf, int vbuf) -> u32x4 {
+    constexpr int NQ = decltype(nq)::value;
+    if (t < NQ) {
       const int kk = t >> 1, beta = t & 1;
       return ld16(&sm.k[kbuf][kread + beta * 2 * SLAB + kk * 256]);
     }
-    const int f = t - NQK;
+    const int f = t - NQ;
     const int beta = f / (2 * DB), u = (f / DB) & 1, db = f % DB;
     return ld16(&sm.v[vbuf][(2 * beta + u) * SLAB + vread + db * 512]);
   };
-  auto fused_block = [&](int kbuf, int vbuf, u32x4 (&fr)[8], f32x16 (&sc)[2],
-                         const bf16x8 (&pprev)[2][2], f32x16 (&cur)[2], bf16x8 (&pcur)[2][2],
-                         float (&sum)[8]) {
+  auto block = [&](auto qk, auto pv, auto smx, auto pre, int kbuf, int vbuf, u32x4 (&fr)[8],
+                   f32x16 (&sc)[2], const bf16x8 (&pw)[2][2], const f32x16 (&cur)[2],
+                   bf16x8 (&pcur)[2][2], float (&sum)[8]) {
+    constexpr bool QK = decltype(qk)::value, PV = decltype(pv)::value;
+    constexpr bool SM = decltype(smx)::value, PRE = decltype(pre)::value;
+    constexpr int NQ = QK ? 2 * KK : 0;
+    constexpr int NOPS = NQ + (PV ? 4 * DB : 0);
+    constexpr int NSUB = NOPS / kSub;
+    constexpr int SLICES = SM ? 16 / NSUB : 0;  // softmax slices per sub-block
+    static_assert(NOPS % kSub == 0 && NOPS > kAhead && kAhead < 8 && (!SM || 16 % NSUB == 0),
+                  "block shape");
+    using nq_t = std::integral_constant<int, NQ>;
+    if constexpr (PRE) {
+#pragma unroll
+      for (int t = 0; t < kAhead; ++t) fr[t] = frag(nq_t(), t, kbuf, vbuf);
+    }
     const float neg_m = -m;
     u32x4 w[2][2];
 #pragma unroll
@@ -353,14 +336,14 @@ __device__ __forceinline__ void prefill_item(
 #pragma unroll
       for (int k = 0; k < kSub; ++k) {
         const int t = kSub * s + k;
-        if (t + kAhead < NOPS) fr[(t + kAhead) & 7] = frag(t + kAhead, kbuf, vbuf);
-        if (t < NQK) {
+        if (t + kAhead < NOPS) fr[(t + kAhead) & 7] = frag(nq_t(), t + kAhead, kbuf, vbuf);
+        if (t < NQ) {
           const int kk = t >> 1, beta = t & 1;
           sc[beta] = mfma32(as_bf16x8(fr[t & 7]), qf[kk], sc[beta]);
         } else {
-          const int f = t - NQK;
+          const int f = t - NQ;
           const int beta = f / (2 * DB), u = (f / DB) & 1, db = f % DB;
-          o[db] = mfma32(as_bf16x8(fr[t & 7]), pprev[beta][u], o[db]);
+          o[db] = mfma32(as_bf16x8(fr[t & 7]), pw[beta][u], o[db]);
         }
       }
 #pragma unroll
@@ -378,23 +361,33 @@ __device__ __forceinline__ void prefill_item(
       for (int k = 0; k < kSub; ++k) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
-        __builtin_amdgcn_sched_group_barrier(0x002, kValu, 0);  // vector ops
+        if constexpr (SM) __builtin_amdgcn_sched_group_barrier(0x002, kValu, 0);  // vector ops
       }
       __builtin_amdgcn_sched_barrier(0);
     }
+    if constexpr (SM) {
+#pragma unroll
+      for (int beta = 0; beta < 2; ++beta)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) pcur[beta][u] = as_bf16x8(w[beta][u]);
+    }
+  };
+  auto zero_scores = [&](f32x16 (&sc)[2]) {
 #pragma unroll
     for (int beta = 0; beta < 2; ++beta)
 #pragma unroll
-      for (int u = 0; u < 2; ++u) pcur[beta][u] = as_bf16x8(w[beta][u]);
+      for (int r = 0; r < 16; ++r) sc[beta][r] = 0.f;
   };
 
   // One step of the software pipeline, for tile kt. On entry cur holds the raw scores of
   // tile kt and pprev the weights of tile kt-1 (when has_prev). One straight-line block
   // then issues the score MFMAs of tile kt+1 (when has_next) and the value MFMAs of tile
-  // kt-1, interleaved with the softmax of tile kt, whose weights use the running maximum m
-  // speculatively: with the lazy rescale m almost never moves, and when some column's
-  // maximum does grow by more than the threshold (always on the first tile, m = -inf) a
-  // rare branch rescales the accumulator and recomputes the weights.
+  // kt-1 (when has_prev), interleaved with the softmax of tile kt, whose weights use the
+  // running maximum m speculatively: with the lazy rescale m almost never moves, and when
+  // some column's maximum does grow by more than the threshold a rare branch rescales the
+  // accumulator and recomputes the weights. On the item's first tile (no has_prev) m is still
+  // -inf: the block only issues the next tile's score products, and the weights follow the
+  // maximum.
   // LDS: step kt reads K(kt+1) from K buffer (kt+1)&1 and V(kt-1) from V buffer (kt-1)&1,
   // and loads K(kt+2) into K buffer kt&1 and V(kt) into V buffer kt&1 -- the buffers whose
   // last readers were in step kt-1, which the barrier at the top of step kt has retired
@@ -403,38 +396,43 @@ __device__ __forceinline__ void prefill_item(
                   bf16x8 (&pprev)[2][2], bf16x8 (&pcur)[2][2]) {
     wait_vmem();
     __syncthreads();  // K(kt+1) and V(kt-1) have landed; all waves are done with step kt-1
-    constexpr bool kFused = decltype(has_next)::value && decltype(has_prev)::value;
+    constexpr bool HN = decltype(has_next)::value, HP = decltype(has_prev)::value;
+    using nq_t = std::integral_constant<int, HN ? 2 * KK : 0>;
     u32x4 fr[8];
-    if constexpr (kFused) {
-      // the first sub-block's K fragments, ahead of the staging issue
+    if constexpr (HN || HP) {
+      // the block's first fragments, ahead of the staging issue
       if (wave_live) {
 #pragma unroll
-        for (int t = 0; t < kAhead; ++t) fr[t] = frag(t, (kt + 1) & 1, (kt - 1) & 1);
+        for (int t = 0; t < kAhead; ++t) fr[t] = frag(nq_t(), t, (kt + 1) & 1, (kt - 1) & 1);
       }
     }
     if (kt + 2 < kt_end) issue_k(kt + 2, kt & 1);
-    if constexpr (decltype(has_prev)::value) issue_v(kt, kt & 1);  // V(0): prologue
+    if constexpr (HP) issue_v(kt, kt & 1);  // V(0): prologue
     if (!wave_live) return;
     const int key0 = kt * kKeys;
     if (key0 + kKeys - 1 > p + wj_lo) mask_tile(key0, cur);
 
-    // ---- the straight-line block (the fenced sub-blocks above in the steady state) ----
+    // ---- the straight-line block ----
     // (at a raised wave priority: when both waves on a SIMD can issue, the one in its block of
     // matrix-core work goes first; 1-1.6% faster on the Llama-3-8B and 70B-shaped layers)
     __builtin_amdgcn_s_setprio(2);
-    float lnew;
-    if constexpr (kFused) {
-      float sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    float lnew = 0.f;
+    float sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if constexpr (HN) zero_scores(nxt);
+    if constexpr (HP) {
+      block(has_next, yes_t(), yes_t(), no_t(), (kt + 1) & 1, (kt - 1) & 1, fr, nxt, pprev,
+            cur, pcur, sum);
+      lnew = ((sum[0] + sum[1]) + (sum[2] + sum[3])) + ((sum[4] + sum[5]) + (sum[6] + sum[7]));
+    } else {
+      // the item's first tile: the running maximum is still -inf, so its weights are computed
+      // below, after the maximum; until then they are zero
+      if constexpr (HN)
+        block(yes_t(), no_t(), no_t(), no_t(), (kt + 1) & 1, 0, fr, nxt, pprev, cur, pcur, sum);
+      const u32x4 zero = {0u, 0u, 0u, 0u};
 #pragma unroll
       for (int beta = 0; beta < 2; ++beta)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) nxt[beta][r] = 0.f;
-      fused_block((kt + 1) & 1, (kt - 1) & 1, fr, nxt, pprev, cur, pcur, sum);
-      lnew = ((sum[0] + sum[1]) + (sum[2] + sum[3])) + ((sum[4] + sum[5]) + (sum[6] + sum[7]));
-    } else {
-      if constexpr (decltype(has_next)::value) scores((kt + 1) & 1, nxt);
-      if constexpr (decltype(has_prev)::value) values((kt - 1) & 1, pprev);
-      lnew = weights(cur, pcur);
+        for (int u = 0; u < 2; ++u) pcur[beta][u] = as_bf16x8(zero);
     }
     // keep the speculative weights in this block: without a use here the compiler would sink
     // their computation past the rare branch below (which overwrites them), out of reach of
@@ -494,7 +492,12 @@ __device__ __forceinline__ void prefill_item(
   __syncthreads();
   f32x16 sa[2], sb[2];
   bf16x8 pa[2][2], pb[2][2];
-  if (wave_live) scores(0, sa);
+  if (wave_live) {
+    u32x4 fr[8];
+    float sum[8];
+    zero_scores(sa);
+    block(yes_t(), no_t(), no_t(), yes_t(), 0, 0, fr, sa, pa, sb, pb, sum);
+  }
   using yes = std::true_type;
   using no = std::false_type;
   // step kt consumes scores sa/sb alternately and writes weights pa/pb alternately
@@ -546,8 +549,10 @@ __device__ __forceinline__ void prefill_item(
       __syncthreads();
     }
     if (wave_live) {
-      if (nt & 1) values(kt & 1, pa);
-      else values(kt & 1, pb);
+      u32x4 fr[8];
+      float sum[8];
+      if (nt & 1) block(no_t(), yes_t(), no_t(), yes_t(), 0, kt & 1, fr, sa, pa, sb, pb, sum);
+      else block(no_t(), yes_t(), no_t(), yes_t(), 0, kt & 1, fr, sa, pb, sb, pa, sum);
     }
   }
 
