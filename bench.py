@@ -447,10 +447,18 @@ def secondary(args, lib, torch, flush):
            lambda: lib.pkv_prefill_attention(pk, pv, b.q, dv["tables"], dv["cached"], dv["cu"],
                                              dv["max_new"], dv["max_total"], wl.scale, o)]
     _, step, per = time_steps(torch, stream, fns, steps, warm, flush)
+    # the same step captured in a HIP graph (the library's calls launch on the current stream
+    # and neither synchronise nor allocate), timed as one replay per step
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for fn in fns:
+            fn()
+    _, gstep, _ = time_steps(torch, stream, [graph.replay], steps, warm, flush)
     out[spec.name] = {"step_us": dist(step, 1e6), "append_us": dist(per[:, 0], 1e6),
                       "prefill_us": dist(per[:, 1], 1e6),
+                      "graph_replay_step_us": dist(gstep, 1e6),
                       "note": "launch-latency bound (34 MFLOP); no roofline claim"}
-    del wl, pk, pv
+    del wl, pk, pv, graph
 
     # Llama-3-8B prefix-reuse prefill step (+ the first decode step)
     spec = W.LLAMA3_8B_PREFILL
@@ -877,7 +885,8 @@ def summary(res):
     t = sec.get("tiny_prefix_reuse_prefill")
     if t:
         log(f"[summary] tiny: step {t['step_us']['median']:.1f} us (append "
-            f"{t['append_us']['median']:.1f}, prefill {t['prefill_us']['median']:.1f})")
+            f"{t['append_us']['median']:.1f}, prefill {t['prefill_us']['median']:.1f}); as a "
+            f"HIP graph replay {t['graph_replay_step_us']['median']:.1f} us")
     s = sec.get("llama3_8b_prefix_reuse_prefill")
     if s:
         log(f"[summary] llama3_8b prefix reuse: {s['tuples_per_s']:.0f} tuples/s, prefill "
