@@ -1,7 +1,8 @@
 """GPU tier: serving steps captured in a HIP graph and replayed.
 
-The library's device calls launch on the caller's stream and make no host synchronisation,
-allocation or memset on the way, so a caller can capture a whole step (here with
+The library's append and attention calls launch on the caller's stream and make no host
+synchronisation, allocation or memset on the way (with the opt-in PKV_DEBUG_VALIDATE checks
+off), so a caller can capture a whole step (here with
 torch.cuda.CUDAGraph, whose capture stream is the current stream the bindings pass on):
   * the decode step: the one-token append, then the allocation-free decode (its workspace is
     the library's fixed per-GPU array, so the graph holds no allocation of its own);
