@@ -7,7 +7,8 @@ torch.cuda.CUDAGraph, whose capture stream is the current stream the bindings pa
   * the decode step: the one-token append, then the allocation-free decode (its workspace is
     the library's fixed per-GPU array, so the graph holds no allocation of its own);
   * the mixed-layer step: the suffix append, the decode-token append, then the fused mixed
-    launch with a workspace allocated before the capture.
+    launch with a workspace allocated before the capture;
+  * the suffix append and the prefill with its plan (ordering, key-split and merge kernels).
 Each graph is replayed three times with fresh inputs copied into its static buffers in
 between (eager copies and a synchronisation between replays). Every replay must equal, bit for
 bit, the same calls made eagerly on a copy of the pool, pools included, and meet the oracle's
@@ -169,3 +170,63 @@ def test_mixed_step_graph_replays(gpu_lib):
             compare("replay 1 decode vs oracle", bf16_to_f64(to_host_bits(out_s[2])), do)
             compare("replay 1 decode lse vs oracle", out_s[3].cpu().numpy().astype(np.float64),
                     dl, atol_max=LSE_MAX, atol_mean=LSE_MEAN)
+
+
+def test_prefill_plan_graph_replays(gpu_lib):
+    """The prefill with its plan (key split and merge, longest-first order; three launches)
+    after the suffix append, captured and replayed."""
+    import torch
+    from tests.test_gpu_prefill import _edge_spec
+    lib = gpu_lib
+    spec = _edge_spec("graph_plan", 241, 32, 8, 128, 3)
+    case = W.make_case(spec, prefix_override=[[9000, 5100, 2600]], new_override=[[37, 150, 90]])
+    b = case.batches[0]
+    pk, pv = dev_pools(case)
+    pk_e, pv_e = pk.clone(), pv.clone()
+    db = DevBatch(b)
+    scale = scale_for(case.d)
+    nbytes = lib.pkv_prefill_workspace_bytes(b.n_seqs, b.total_new, case.hq, case.hkv, case.d,
+                                             db.max_new, db.max_total)
+    say(f"[graph] prefill with its plan: {b.n_seqs} tuples, workspace {nbytes} B")
+    assert nbytes > 256, "the case was meant to split its keys"
+    ws, ws_e = lib.alloc_workspace(nbytes), lib.alloc_workspace(nbytes)
+    ins_s = [db.q.clone(), db.k_new.clone(), db.v_new.clone()]
+    out_s = [torch.empty((b.total_new, case.hq, case.d), dtype=torch.bfloat16, device="cuda"),
+             torch.empty((b.total_new, case.hq), dtype=torch.float32, device="cuda")]
+    out_e = [torch.empty_like(t) for t in out_s]
+
+    def step(pool_k, pool_v, ins, o, w):
+        q, kn, vn = ins
+        lib.pkv_kv_append(pool_k, pool_v, kn, vn, db.tables, db.cached, db.cu, db.max_new)
+        lib.pkv_prefill_attention(pool_k, pool_v, q, db.tables, db.cached, db.cu, db.max_new,
+                                  db.max_total, scale, o[0], lse=o[1], workspace=w)
+
+    step(pk, pv, ins_s, out_s, ws)
+    step(pk_e, pv_e, ins_s, out_e, ws_e)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step(pk, pv, ins_s, out_s, ws)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(2609)
+    for r in range(REPLAYS):
+        ins = [_fresh(gen, t) for t in ins_s]
+        for dst, src in zip(ins_s, ins):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        step(pk_e, pv_e, ins, out_e, ws_e)
+        torch.cuda.synchronize()
+        say(f"  replay {r + 1}")
+        assert _bits_equal(out_s[0], out_e[0]), f"replay {r + 1}: output differs"
+        assert _bits_equal(out_s[1], out_e[1]), f"replay {r + 1}: lse differs"
+        assert _bits_equal(pk, pk_e) and _bits_equal(pv, pv_e), f"replay {r + 1}: pools differ"
+        if r == 0:
+            h = [to_host_bits(t) for t in ins]
+            ro, rl = oracle.prefill_attention(case.pool_k, case.pool_v, b.block_tables,
+                                              b.prefix_lens, b.cu_new_lens, h[0], h[1], h[2],
+                                              scale, case.bs)
+            compare("replay 1 vs oracle", bf16_to_f64(to_host_bits(out_s[0])), ro)
+            compare("replay 1 lse vs oracle", out_s[1].cpu().numpy().astype(np.float64), rl,
+                    atol_max=LSE_MAX, atol_mean=LSE_MEAN)
