@@ -62,6 +62,9 @@ SPLIT_CASES = [
     # 8 query heads per kv head, split size 1024: the first token of one sequence ends in the
     # first split (its last key is 1023), the next one does not
     ("gqa8_ragged", 64, 8, 128, [1023, 4100], [17, 260]),
+    # sequences without new tokens (no rows, no work items) between split ones, and keys past
+    # 8192 (so the plan also orders the sequences, the empty ones last)
+    ("empty_rows_ordered", 32, 8, 128, [5000, 0, 9000, 3000, 64], [0, 40, 100, 0, 7]),
 ]
 
 
