@@ -5,7 +5,10 @@ batch size, per-sequence prefix and suffix lengths (prefixes ending anywhere in 
 empty prefixes included) and a random block placement. The append is checked bit for bit
 over the whole pool (every byte outside the new slots unchanged, NaN canaries included),
 prefill and decode against the fp64 oracle at the same bar as the other GPU tests; a sweep of
-small batches of long sequences runs the prefill with its plan (key split, order)."""
+small batches of long sequences runs the prefill with its plan (key split, order).
+PKV_RANDOM_SCALE=n runs n times as many cases (the default sweep is 12 + 12 + 8)."""
+import os
+
 import numpy as np
 import pytest
 
@@ -20,6 +23,7 @@ from tests.test_gpu_prefill import oracle_prefill, run_prefill
 pytestmark = pytest.mark.gpu
 
 SEED = 260723815 + 900
+SCALE = max(1, int(os.environ.get("PKV_RANDOM_SCALE", "1")))
 
 
 def _heads(rng):
@@ -55,7 +59,7 @@ def _decode_case(k):
     return W.make_case(spec, prefix_override=[ctx.tolist()])
 
 
-@pytest.mark.parametrize("k", range(12))
+@pytest.mark.parametrize("k", range(12 * SCALE))
 def test_random_prefill_and_append(gpu_lib, k):
     case = _prefill_case(k)
     b = case.batches[0]
@@ -73,7 +77,7 @@ def test_random_prefill_and_append(gpu_lib, k):
                   oracle_prefill(case))
 
 
-@pytest.mark.parametrize("k", range(12))
+@pytest.mark.parametrize("k", range(12 * SCALE))
 def test_random_decode(gpu_lib, k):
     case = _decode_case(k)
     b = case.batches[0]
@@ -97,7 +101,7 @@ def _plan_case(k):
                        new_override=[news.tolist()])
 
 
-@pytest.mark.parametrize("k", range(8))
+@pytest.mark.parametrize("k", range(8 * SCALE))
 def test_random_prefill_with_plan(gpu_lib, k):
     """Random small batches of long sequences through the prefill with the plan's workspace
     (key split, longest-first order) against the oracle."""
