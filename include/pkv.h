@@ -442,7 +442,9 @@ typedef struct {
 
 /* Device mode: each engine step also runs its attention work on the GPU through this
  * library's calls (block copies for copy-on-write, KV append, prefill attention for tasks in
- * their first step, decode attention for the others), on `stream`, timed with HIP events. The
+ * their first step, decode attention for the others; a step with both sends its last prefill
+ * group and its decode group out together as one pkv_mixed_attention launch), on `stream`,
+ * timed with HIP events. The
  * step's K/V rows and queries are read from rows 0.. of the caller's synthetic sources
  * (bf16 [src_rows][num_kv_heads][head_dim] and [src_rows][num_q_heads][head_dim]; src_rows
  * >= max_batch and >= the longest prefix plus suffix of any task, checked before anything
@@ -467,7 +469,9 @@ typedef struct {
 } pkv_sched_group;
 /* Optional observer of device mode (tests, tracing): called on the calling thread twice per
  * group of sequences launched together, with the stream drained; it may read the pool and the
- * output but must not modify them. */
+ * output but must not modify them. When a prefill group and a decode group go out in one
+ * fused launch, both phase-0 calls (prefill first) come before both phase-1 calls, and each
+ * group's output is at its own address. */
 typedef void (*pkv_sched_group_hook)(void* user, const pkv_sched_group* group);
 
 typedef struct {

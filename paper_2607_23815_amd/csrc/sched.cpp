@@ -82,8 +82,9 @@ class DeviceRunner {
       return pkv::fail(PKV_ERR_INVALID_ARG, "pkv_sched_run: src_rows < max_batch");
     max_table_ = max_table;
     max_batch_ = max_batch;
-    const size_t meta_ints = (size_t)max_batch * max_table + 4 * (size_t)max_batch + 8 +
-                             2 * (size_t)max_batch;
+    // room for two groups' metadata (a step's last prefill group and its decode group go out
+    // together), or for max_batch copy-on-write pairs
+    const size_t meta_ints = 2 * ((size_t)max_batch * max_table + 4 * (size_t)max_batch + 8);
     meta_bytes_ = meta_ints * sizeof(int32_t);
     // The decode workspace depends on the batch and the longest sequence, and not
     // monotonically in the latter (shorter sequences may split into more pieces). Size it for
@@ -98,7 +99,10 @@ class DeviceRunner {
       ws = std::max(ws, order + parts);
     }
     ws_bytes_ = ws;
-    const size_t out_bytes = (size_t)dev_.src_rows * dev_.num_q_heads * kv.head_dim * 2;
+    // prefill rows (at most src_rows), then a decode group's rows (at most max_batch)
+    out_dec_off_ = (size_t)dev_.src_rows * dev_.num_q_heads * kv.head_dim * 2;
+    const size_t out_bytes =
+        out_dec_off_ + (size_t)max_batch * dev_.num_q_heads * kv.head_dim * 2;
     hipError_t e = hipMalloc(&meta_dev_, meta_bytes_);
     if (e == hipSuccess) e = hipHostMalloc(&meta_host_, meta_bytes_, hipHostMallocDefault);
     if (e == hipSuccess) e = hipMalloc(&out_, out_bytes);
@@ -135,13 +139,15 @@ class DeviceRunner {
       if (st != PKV_OK) return st;
       if ((st = end_segment()) != PKV_OK) return st;
     }
-    // prefill: groups of at most src_rows new tokens
+    // prefill: groups of at most src_rows new tokens; the last one goes out with the decode
+    // group in one fused launch (pkv_mixed_attention) when the step has both
     size_t a = 0;
     while (a < pre.size()) {
       size_t b = a;
       int64_t rows = 0;
       while (b < pre.size() && rows + pre[b].n_new <= dev_.src_rows) rows += pre[b++].n_new;
       if (b == a) return pkv::fail(PKV_ERR_INVALID_ARG, "pkv_sched_run: a prompt exceeds src_rows");
+      if (b == pre.size() && !dec.empty()) return run_fused(pool, pre, a, b, dec);
       if ((st = run_group(pool, pre, a, b, false)) != PKV_OK) return st;
       a = b;
     }
@@ -166,7 +172,7 @@ class DeviceRunner {
   }
 
   void call_hook(int32_t phase, bool decode, int32_t n, const int32_t* tab, const int32_t* cached,
-                 const int32_t* cu) {
+                 const int32_t* cu, const void* out) {
     if (dev_.group_hook == nullptr) return;
     pkv_sched_group g;
     g.step = step_no_;
@@ -177,12 +183,55 @@ class DeviceRunner {
     g.tables = tab;
     g.cached = cached;
     g.cu_new = cu;
-    g.out = out_;
+    g.out = out;
     dev_.group_hook(dev_.hook_user, &g);
   }
 
   hipError_t upload(const int32_t* h, int32_t* d, size_t n, hipStream_t stream) {
     return hipMemcpyAsync(d, h, n * sizeof(int32_t), hipMemcpyHostToDevice, stream);
+  }
+
+  // One group's launch metadata, laid out at `h` (host, pinned) and mirrored at `d` (device):
+  // tables [n][max_table], cached [n], cu_new [n + 1], lens [n].
+  struct Group {
+    int32_t n = 0, rows = 0, max_new = 0, max_total = 0;
+    int32_t *h_tab = nullptr, *h_cached = nullptr, *h_cu = nullptr, *h_lens = nullptr;
+    const int32_t *d_tab = nullptr, *d_cached = nullptr, *d_cu = nullptr, *d_lens = nullptr;
+    size_t ints = 0;  // metadata size
+  };
+  pkv_status fill_group(pkv_pool* pool, const std::vector<StepItem>& items, size_t a, size_t b,
+                        int32_t* h, const int32_t* d, Group* g) {
+    const int32_t n = (int32_t)(b - a);
+    g->n = n;
+    g->h_tab = h;
+    g->h_cached = h + (size_t)n * max_table_;
+    g->h_cu = g->h_cached + n;
+    g->h_lens = g->h_cu + n + 1;
+    g->d_tab = d;
+    g->d_cached = d + (size_t)n * max_table_;
+    g->d_cu = g->d_cached + n;
+    g->d_lens = g->d_cu + n + 1;
+    g->ints = (size_t)n * max_table_ + 3 * (size_t)n + 1;
+    std::vector<int64_t> ids((size_t)n);
+    g->max_new = g->max_total = 0;
+    for (int32_t k = 0; k < n; ++k) {
+      const StepItem& it = items[a + k];
+      ids[k] = it.seq;
+      g->h_cached[k] = it.cached;
+      g->h_cu[k] = k == 0 ? 0 : g->h_cu[k - 1] + items[a + k - 1].n_new;
+      g->h_lens[k] = it.cached + it.n_new;
+      g->max_new = std::max(g->max_new, it.n_new);
+      g->max_total = std::max(g->max_total, it.cached + it.n_new);
+    }
+    g->h_cu[n] = g->h_cu[n - 1] + items[b - 1].n_new;
+    g->rows = g->h_cu[n];
+    return pkv_fill_block_tables(pool, ids.data(), n, max_table_, g->h_tab, nullptr);
+  }
+
+  // The group's KV append (rows cu_new[k].. of the K/V sources)
+  pkv_status append(const Group& g) {
+    return pkv_kv_append(&dev_.kv, dev_.k_src, dev_.v_src, g.d_tab, max_table_, g.d_cached,
+                         g.d_cu, g.n, g.rows, g.max_new, dev_.stream);
   }
 
   // Metadata of items [a, b) into the pinned staging area and the device copy, then the
@@ -191,55 +240,68 @@ class DeviceRunner {
   pkv_status run_group(pkv_pool* pool, const std::vector<StepItem>& items, size_t a, size_t b,
                        bool decode) {
     hipStream_t stream = static_cast<hipStream_t>(dev_.stream);
-    const int32_t n = (int32_t)(b - a);
     int32_t* h = static_cast<int32_t*>(meta_host_);
     int32_t* d = static_cast<int32_t*>(meta_dev_);
-    int32_t* h_tab = h;
-    int32_t* h_cached = h_tab + (size_t)n * max_table_;
-    int32_t* h_cu = h_cached + n;
-    int32_t* h_lens = h_cu + n + 1;
-    std::vector<int64_t> ids((size_t)n);
-    int32_t max_new = 0, max_total = 0;
-    for (int32_t k = 0; k < n; ++k) {
-      const StepItem& it = items[a + k];
-      ids[k] = it.seq;
-      h_cached[k] = it.cached;
-      h_cu[k] = k == 0 ? 0 : h_cu[k - 1] + items[a + k - 1].n_new;
-      h_lens[k] = it.cached + it.n_new;
-      max_new = std::max(max_new, it.n_new);
-      max_total = std::max(max_total, it.cached + it.n_new);
-    }
-    h_cu[n] = h_cu[n - 1] + items[b - 1].n_new;
-    pkv_status st = pkv_fill_block_tables(pool, ids.data(), n, max_table_, h_tab, nullptr);
+    Group g;
+    pkv_status st = fill_group(pool, items, a, b, h, d, &g);
     if (st != PKV_OK) return st;
-    const size_t total = (size_t)n * max_table_ + 3 * (size_t)n + 1;
-    hipError_t e = upload(h, d, total, stream);
+    hipError_t e = upload(h, d, g.ints, stream);
     if (e != hipSuccess) return hip_fail(e);
     if (dev_.group_hook != nullptr) {  // the pool and the metadata settle before the hook
       if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e);
-      call_hook(0, decode, n, h_tab, h_cached, h_cu);
+      call_hook(0, decode, g.n, g.h_tab, g.h_cached, g.h_cu, out_);
     }
     if ((e = hipEventRecord(ev0_, stream)) != hipSuccess) return hip_fail(e);
-    const int32_t* d_tab = d;
-    const int32_t* d_cached = d_tab + (size_t)n * max_table_;
-    const int32_t* d_cu = d_cached + n;
-    const int32_t* d_lens = d_cu + n + 1;
-    const int32_t rows = h_cu[n];
-    st = pkv_kv_append(&dev_.kv, dev_.k_src, dev_.v_src, d_tab, max_table_, d_cached, d_cu, n,
-                       rows, max_new, dev_.stream);
-    if (st != PKV_OK) return st;
+    if ((st = append(g)) != PKV_OK) return st;
     const float scale = 1.0f / std::sqrt((float)dev_.kv.head_dim);
     if (decode)
-      st = pkv_decode_attention(&dev_.kv, dev_.q_src, dev_.num_q_heads, d_tab, max_table_,
-                                d_lens, n, max_total, scale, out_, nullptr, ws_, ws_bytes_,
-                                dev_.stream);
+      st = pkv_decode_attention(&dev_.kv, dev_.q_src, dev_.num_q_heads, g.d_tab, max_table_,
+                                g.d_lens, g.n, g.max_total, scale, out_, nullptr, ws_,
+                                ws_bytes_, dev_.stream);
     else
-      st = pkv_prefill_attention(&dev_.kv, dev_.q_src, dev_.num_q_heads, d_tab, max_table_,
-                                 d_cached, d_cu, n, rows, max_new, max_total, scale, out_,
-                                 nullptr, nullptr, 0, dev_.stream);
+      st = pkv_prefill_attention(&dev_.kv, dev_.q_src, dev_.num_q_heads, g.d_tab, max_table_,
+                                 g.d_cached, g.d_cu, g.n, g.rows, g.max_new, g.max_total, scale,
+                                 out_, nullptr, nullptr, 0, dev_.stream);
     if (st != PKV_OK) return st;
     if ((st = end_segment()) != PKV_OK) return st;
-    call_hook(1, decode, n, h_tab, h_cached, h_cu);
+    call_hook(1, decode, g.n, g.h_tab, g.h_cached, g.h_cu, out_);
+    return PKV_OK;
+  }
+
+  // The prefill group of items pre[a, b) and the decode group dec together: one metadata
+  // upload, both appends, then one fused launch (pkv_mixed_attention, bit-identical to the
+  // prefill call followed by the decode call). The prefill output goes to the start of the
+  // output buffer, the decode output after the src_rows rows a prefill group can fill.
+  pkv_status run_fused(pkv_pool* pool, const std::vector<StepItem>& pre, size_t a, size_t b,
+                       const std::vector<StepItem>& dec) {
+    hipStream_t stream = static_cast<hipStream_t>(dev_.stream);
+    int32_t* h = static_cast<int32_t*>(meta_host_);
+    int32_t* d = static_cast<int32_t*>(meta_dev_);
+    Group gp, gd;
+    pkv_status st = fill_group(pool, pre, a, b, h, d, &gp);
+    if (st != PKV_OK) return st;
+    st = fill_group(pool, dec, 0, dec.size(), h + gp.ints, d + gp.ints, &gd);
+    if (st != PKV_OK) return st;
+    hipError_t e = upload(h, d, gp.ints + gd.ints, stream);
+    if (e != hipSuccess) return hip_fail(e);
+    void* out_dec = static_cast<char*>(out_) + out_dec_off_;
+    if (dev_.group_hook != nullptr) {  // both groups' pool blocks and metadata, before the appends
+      if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e);
+      call_hook(0, false, gp.n, gp.h_tab, gp.h_cached, gp.h_cu, out_);
+      call_hook(0, true, gd.n, gd.h_tab, gd.h_cached, gd.h_cu, out_dec);
+    }
+    if ((e = hipEventRecord(ev0_, stream)) != hipSuccess) return hip_fail(e);
+    if ((st = append(gp)) != PKV_OK) return st;
+    if ((st = append(gd)) != PKV_OK) return st;
+    const float scale = 1.0f / std::sqrt((float)dev_.kv.head_dim);
+    st = pkv_mixed_attention(&dev_.kv, dev_.num_q_heads, scale, dev_.q_src, gp.d_tab, max_table_,
+                             gp.d_cached, gp.d_cu, gp.n, gp.rows, gp.max_new, gp.max_total,
+                             out_, nullptr, dev_.q_src, gd.d_tab, max_table_, gd.d_lens, gd.n,
+                             gd.max_total, out_dec, nullptr, ws_, ws_bytes_, dev_.stream);
+    if (st != PKV_OK) return st;
+    if ((st = end_segment()) != PKV_OK) return st;
+    call_hook(1, false, gp.n, gp.h_tab, gp.h_cached, gp.h_cu, out_);
+    call_hook(1, true, gd.n, gd.h_tab, gd.h_cached, gd.h_cu, out_dec);
     return PKV_OK;
   }
 
@@ -260,7 +322,7 @@ class DeviceRunner {
   int64_t step_no_ = 0;
   double* ms_ = nullptr;
   int32_t max_table_ = 0, max_batch_ = 0;
-  size_t meta_bytes_ = 0, ws_bytes_ = 0;
+  size_t meta_bytes_ = 0, ws_bytes_ = 0, out_dec_off_ = 0;
   void* meta_dev_ = nullptr;
   void* meta_host_ = nullptr;
   void* out_ = nullptr;

@@ -115,7 +115,7 @@ def test_device_mode_results_match_the_oracle(gpu_lib, pidx, policy, budget):
     def hook(g):
         dec = g["decode"]
         if g["phase"] == 0:
-            state.pop("cur", None)
+            state.pop(dec, None)
             k = seen[dec]
             seen[dec] += 1
             cached, cu = g["cached"], g["cu_new"]
@@ -126,11 +126,11 @@ def test_device_mode_results_match_the_oracle(gpu_lib, pidx, policy, budget):
             used = [g["tables"][s, :-(-(int(cached[s]) + int(n_new[s])) // 16)]
                     for s in range(len(cached))]
             ids = np.unique(np.concatenate(used))
-            state["cur"] = (g, ids, blocks(ids))
+            state[dec] = (g, ids, blocks(ids))
             return
-        if "cur" not in state:
+        if dec not in state:
             return
-        g0, ids, (bk, bv) = state.pop("cur")
+        g0, ids, (bk, bv) = state.pop(dec)
         try:
             cached, cu = g0["cached"], g0["cu_new"]
             n = len(cached)
