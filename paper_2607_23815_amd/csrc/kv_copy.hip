@@ -20,11 +20,6 @@
 namespace pkv {
 namespace {
 
-// 16-byte store with the non-temporal hint (streaming data not read again by this launch).
-__device__ __forceinline__ void st16_nt(void* p, u32x4 v) {
-  __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
-}
-
 template <int D>
 __global__ __launch_bounds__(256) void kv_append_kernel(
     const uint16_t* __restrict__ k_new, const uint16_t* __restrict__ v_new,

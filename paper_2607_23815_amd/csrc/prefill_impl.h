@@ -558,7 +558,9 @@ __device__ __forceinline__ void prefill_item(
 
   const float l = lpart + swap_halves(lpart);
   if (!wave_live) return;
-  // The wave's 32 output rows go out through LDS as whole rows: a lane holds 8-byte pieces
+  // The wave's 32 output rows go out through LDS as whole rows, with non-temporal stores (so
+  // that no dirty lines of the output are left for later work to write back; a launch's output
+  // is mostly larger than the memory-side cache anyway): a lane holds 8-byte pieces
   // of one row (column), so storing them directly would put 32 rows into every store
   // instruction; written to LDS first (the K buffers, free since the last step's barrier:
   // 32 rows x D per wave), each 16-byte store below covers 64 / (D / 8) complete rows.
@@ -619,7 +621,7 @@ __device__ __forceinline__ void prefill_item(
     const int gc = wcol0 + r;
     if (gc < ncols && row_ends_here(gc)) {
       const int jr = gc / g;
-      st16(out + ((size_t)(row0 + jr) * hq + kvh * g + gc % g) * D + u * 8, v);
+      st16_nt(out + ((size_t)(row0 + jr) * hq + kvh * g + gc % g) * D + u * 8, v);
     }
   }
   const int gcl = wcol0 + lcl;  // this lane's column, recomputed like the lane index
