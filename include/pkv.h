@@ -275,17 +275,22 @@ pkv_status pkv_kv_append(const pkv_paged_kv* kv, const void* k_new, const void* 
  * work items; a row whose keys end in the first part is finished there, the others are
  * merged from their parts' partial results by log-sum-exp weights in a second kernel. The
  * cut points depend on key positions and host arguments only, so results are
- * deterministic. With workspace NULL (or when the size is 0) the launch does not split; a
- * non-NULL workspace smaller than the size is refused. Calls sharing a workspace must not
- * overlap. */
+ * deterministic. Order (optional, the same workspace): a batch of more than one sequence
+ * whose keys reach 8192 (max_total_len >= 8192) takes its sequences longest first (a small
+ * kernel writes the order into the workspace), so the launch does not end on a few long
+ * items; the order moves work items, not arithmetic, so the results are bit-identical to
+ * the unordered launch. With workspace NULL (or when the size is 0) the launch neither
+ * splits nor orders; a non-NULL workspace smaller than the size is refused. Calls sharing a
+ * workspace must not overlap. */
 pkv_status pkv_prefill_attention(const pkv_paged_kv* kv, const void* q, int32_t num_q_heads,
                                  const int32_t* block_tables, int32_t max_blocks,
                                  const int32_t* cached_lens, const int32_t* cu_new_lens,
                                  int32_t num_seqs, int32_t total_new, int32_t max_new_len,
                                  int32_t max_total_len, float scale, void* out, float* lse,
                                  void* workspace, size_t workspace_bytes, void* stream);
-/* Workspace that enables the prefill's key split: total_new x num_q_heads x splits x
- * (head_dim + 2) floats when the batch splits, else 0. */
+/* Workspace that enables the prefill's plan: num_seqs int32 rounded up to 256 bytes when the
+ * batch is ordered, plus total_new x num_q_heads x splits x (head_dim + 2) floats when it
+ * splits; 0 when it does neither (or for arguments the call would refuse). */
 size_t pkv_prefill_workspace_bytes(int32_t num_seqs, int32_t total_new, int32_t num_q_heads,
                                    int32_t num_kv_heads, int32_t head_dim,
                                    int32_t max_new_len, int32_t max_total_len);
