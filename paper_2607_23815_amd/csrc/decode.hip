@@ -79,10 +79,12 @@ constexpr int kOrderThreads = 1024;
 __global__ __launch_bounds__(kOrderThreads) void decode_order_kernel(
     const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ cu, int32_t num_seqs,
     int32_t* __restrict__ order) {
+  constexpr int kWavesO = kOrderThreads / 64;
   __shared__ int count[kOrderBuckets];
   __shared__ int base[kOrderBuckets];
-  __shared__ int part[kOrderThreads];
+  __shared__ int wsum[kWavesO];
   const int t = threadIdx.x;
+  const int lane = t & 63, w = t >> 6;
   for (int b = t; b < kOrderBuckets; b += kOrderThreads) count[b] = 0;
   __syncthreads();
   auto bucket_of = [&](int i) {
@@ -92,18 +94,29 @@ __global__ __launch_bounds__(kOrderThreads) void decode_order_kernel(
   };
   for (int i = t; i < num_seqs; i += kOrderThreads) atomicAdd(&count[bucket_of(i)], 1);
   __syncthreads();
-  // exclusive scan in descending bucket order: thread t owns descending positions 2t, 2t+1
+  // exclusive scan in descending bucket order: thread t owns descending positions 2t, 2t+1;
+  // an inclusive scan within each wave (lane shuffles), then one over the waves' totals
   const int b0 = kOrderBuckets - 1 - 2 * t, b1 = b0 - 1;
   const int c0 = count[b0], c1 = count[b1];
-  part[t] = c0 + c1;
-  __syncthreads();
-  for (int off = 1; off < kOrderThreads; off <<= 1) {
-    const int v = t >= off ? part[t - off] : 0;
-    __syncthreads();
-    part[t] += v;
-    __syncthreads();
+  const int v = c0 + c1;
+  int incl = v;
+  for (int off = 1; off < 64; off <<= 1) {
+    const int u = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += u;
   }
-  const int excl = part[t] - (c0 + c1);
+  if (lane == 63) wsum[w] = incl;
+  __syncthreads();
+  if (w == 0) {
+    const int x = lane < kWavesO ? wsum[lane] : 0;
+    int inc = x;
+    for (int off = 1; off < kWavesO; off <<= 1) {
+      const int u = __shfl_up(inc, off, 64);
+      if (lane >= off) inc += u;
+    }
+    if (lane < kWavesO) wsum[lane] = inc - x;  // waves before this one
+  }
+  __syncthreads();
+  const int excl = wsum[w] + incl - v;
   base[b0] = excl;
   base[b1] = excl + c0;
   __syncthreads();
